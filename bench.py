@@ -1,0 +1,268 @@
+#!/usr/bin/env python3
+"""Throughput of the delta-scatter backbone on one MI355X.
+
+One "step" is one sliding-window stride through the whole hot path: changed
+cell detection on the pillar canvas, then for every layer the delta
+contraction on the matrix cores, the update of the persistent map, the
+activation-delta epilogue and the change-list propagation.
+
+Workload (default): PointPillars block 1 -- one 3x3 stride-2 conv and three
+3x3 stride-1 convs, 64 channels, ReLU, fp32 -- on the 432x496 grid, fed by a
+seeded synthetic sweep stream of ~12k occupied pillars whose 36 degree sector
+is refreshed each stride (~10% of the pillars).  All strides are uploaded to
+HBM before timing; the full window (stride 0) and `warmup` delta strides run
+untimed, then exactly `steps` delta strides are timed.
+
+Printed: one JSON line with
+  value        changed-cell conv updates per second, sum_l |A_{l-1}| per stride
+               (one changed input cell pushed through one layer's 3x3 filter bank)
+  ms_per_step  wall-clock ms per stride over the timed region
+  roofline     the dominant kernel's algorithmic flops (or bytes) per launch over
+               its HIP-event-timed duration, against the MI355X peak
+  cpu_baseline the CPU oracle (dense float64 recompute) on a bounded sample of the
+               same strides
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import streams as S  # noqa: E402
+
+PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}   # dense MFMA peaks of MI355X
+PEAK_HBM_GBS = 8000.0
+METRIC = "ms per stride and changed-cell conv updates/s; fraction of HBM/MFMA roofline"
+
+
+def log(msg: str) -> None:
+    sys.stderr.write(msg + "\n")
+    sys.stderr.flush()
+
+
+def layers_of(wl):
+    return [(l.cin, l.cout, l.stride, bool(l.relu)) for l in wl.layers]
+
+
+def upload(strides, dtype):
+    import torch
+    out = []
+    for st in strides:
+        f = st.feats.view(np.int16) if dtype == "bf16" else st.feats
+        out.append((torch.from_numpy(np.ascontiguousarray(st.idx)).cuda(),
+                    torch.from_numpy(np.ascontiguousarray(f)).cuda()))
+    torch.cuda.synchronize()
+    return out
+
+
+def kernel_name(slot: int, wl) -> str:
+    if slot == 0:
+        return "detect_kernel<present>"
+    if slot == 1:
+        return "detect_kernel<vanished>"
+    l = wl.layers[slot - 2]
+    return f"layer_kernel<{l.cin},{l.cout},{l.stride},{wl.dtype}>"
+
+
+def cpu_baseline(wl, ws, strides, first, budget_s):
+    """The oracle as it stands (dense float64 recompute of every layer plus the
+    change lists) on consecutive strides of the timed range, until the time
+    budget is spent."""
+    import oracle
+    layers = layers_of(wl)
+    prev = oracle.canvas_bits(S.canvas(strides[first - 1], wl.H, wl.W, wl.C0), wl.dtype)
+    t_total, u_total, n = 0.0, 0, 0
+    for st in strides[first:]:
+        canvas = S.canvas(st, wl.H, wl.W, wl.C0)
+        t0 = time.perf_counter()
+        bits = oracle.canvas_bits(canvas, wl.dtype)
+        x = oracle.exact_canvas(canvas, wl.dtype)
+        oracle.forward(x, ws, layers, bf16_storage=(wl.dtype == "bf16"))
+        lists = oracle.changed_lists(prev, bits, [l[2] for l in layers])
+        t_total += time.perf_counter() - t0
+        u_total += sum(len(a) for a in lists[:-1])
+        prev = bits
+        n += 1
+        if t_total >= budget_s:
+            break
+    return {"value": u_total / t_total, "unit": "updates/s", "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"{n} consecutive delta strides of the timed range, each a dense float64 recompute of "
+                      f"all {len(layers)} layers plus the per-layer change lists ({t_total:.1f} s, "
+                      f"{t_total / n * 1e3:.1f} ms per stride)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="c2", choices=sorted(S.WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=20.0, help="time budget of the CPU oracle sample")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        log("bench.py: this build runs on one GPU only; multi-GPU runs are not supported "
+            "(independent sensor streams would shard one per GPU with no communication).")
+        return 2
+    if int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        log("bench.py: launched with WORLD_SIZE > 1; this build runs on one GPU only.")
+        return 2
+
+    import torch
+    from paper_2512_08557_amd import Engine
+
+    torch.cuda.set_device(0)
+    wl = S.workload(args.workload)
+    ws = S.weights(args.workload)
+    K, W = args.steps, args.warmup
+    log(f"[bench] workload {wl.name}: {wl.description}; generating {W + K} delta strides")
+    strides = S.make_stream(wl.name, n_strides=W + K)
+    dev = upload(strides, wl.dtype)
+    eng = Engine(wl.H, wl.W, wl.C0, layers_of(wl), ws, dtype=wl.dtype, max_pillars=wl.max_pillars)
+    L = len(wl.layers)
+
+    def run_range(lo, hi):
+        for k in range(lo, hi):
+            eng.step(*dev[k])
+
+    # full window + warmup (untimed)
+    run_range(0, 1 + W)
+    torch.cuda.synchronize()
+    before = eng.stats()
+
+    # ---- timed region: exactly K delta strides ----
+    stream = torch.cuda.current_stream()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    evs[0].record(stream)
+    for k in range(K):
+        eng.step(*dev[1 + W + k])
+        evs[k + 1].record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    after = eng.stats()
+    wall_ms = (t1 - t0) * 1e3
+    per_stride = [evs[k].elapsed_time(evs[k + 1]) for k in range(K)]
+    act_in = [after["active_total"][l] - before["active_total"][l] for l in range(L + 1)]
+    pairs = [after["pairs_total"][l] - before["pairs_total"][l] for l in range(L + 1)]
+    updates = sum(act_in[:L])          # sum_l |A_{l-1}| over the timed strides
+    ms_per_step = wall_ms / K
+    value = updates / (wall_ms / 1e3)
+    log(f"[bench] {K} strides in {wall_ms:.2f} ms -> {ms_per_step * 1e3:.1f} us/stride, "
+        f"{value:.3e} updates/s; mean |A_l| = {[round(a / K) for a in act_in]}")
+
+    # ---- per-kernel pass: same strides, HIP events around every launch ----
+    roofline = None
+    kernels = {}
+    if not args.no_profile:
+        eng.reset()
+        run_range(0, 1 + W)
+        eng.profile_read()               # drop anything recorded so far
+        b2 = eng.stats()
+        eng.profile(True)
+        run_range(1 + W, 1 + W + K)
+        ms, cnt = eng.profile_read()
+        eng.profile(False)
+        a2 = eng.stats()
+        pairs2 = [a2["pairs_total"][l] - b2["pairs_total"][l] for l in range(L + 1)]
+        act2 = [a2["active_total"][l] - b2["active_total"][l] for l in range(L + 1)]
+        e_d = 4.0
+        for slot in range(L + 2):
+            if cnt[slot] == 0:
+                continue
+            name = kernel_name(slot, wl)
+            k = kernels.setdefault(name, {"ms": 0.0, "launches": 0, "flops": 0.0, "bytes": 0.0})
+            k["ms"] += ms[slot]
+            k["launches"] += cnt[slot]
+            if slot >= 2:
+                l = slot - 1
+                sp = wl.layers[l - 1]
+                k["flops"] += 2.0 * sp.cin * sp.cout * pairs2[l]
+                k["bytes"] += (act2[l - 1] * sp.cin * e_d + act2[l] * sp.cout * 8.0 +
+                               (act2[l] * sp.cout * e_d if l < L else 0.0) +
+                               cnt[slot] * 9.0 * sp.cin * sp.cout * (2 if wl.dtype == "bf16" else 4) +
+                               12.0 * (act2[l - 1] + act2[l]))
+        for name, k in kernels.items():
+            log(f"[bench] {name:34s} {k['launches']:5d} launches  avg {k['ms'] / k['launches'] * 1e3:8.2f} us  "
+                f"total {k['ms']:.3f} ms")
+        dom_name, dom = max(kernels.items(), key=lambda kv: kv[1]["ms"])
+        if dom["flops"] > 0:
+            intensity = dom["flops"] / max(dom["bytes"], 1.0)
+            peak_t = PEAK_TFLOPS[wl.dtype]
+            if intensity >= peak_t * 1e12 / (PEAK_HBM_GBS * 1e9):
+                achieved = dom["flops"] / (dom["ms"] / 1e3) / 1e12
+                roofline = {"bound": "mfma", "achieved": achieved, "peak": peak_t, "unit": "TFLOP/s",
+                            "frac": achieved / peak_t, "traffic": None}
+            else:
+                achieved = dom["bytes"] / (dom["ms"] / 1e3) / 1e9
+                roofline = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                            "frac": achieved / PEAK_HBM_GBS, "traffic": None}
+            roofline.update({"kernel": dom_name, "launches": dom["launches"],
+                             "avg_launch_us": dom["ms"] / dom["launches"] * 1e3,
+                             "alg_flops_per_launch": dom["flops"] / dom["launches"],
+                             "alg_bytes_per_launch": dom["bytes"] / dom["launches"]})
+
+    # ---- GPU full recompute: reset + full window through the same kernels ----
+    full = []
+    last = dev[W + K]
+    for _ in range(5):
+        eng.reset()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        eng.step(*last)
+        b.record(stream)
+        torch.cuda.synchronize()
+        full.append(a.elapsed_time(b))
+    full_ms = statistics.median(full)
+    eng.close()
+
+    cpu = None
+    if not args.no_cpu:
+        try:
+            log(f"[bench] CPU oracle baseline (budget {args.cpu_seconds:.0f} s)")
+            cpu = cpu_baseline(wl, ws, strides, 1 + W, args.cpu_seconds)
+        except Exception as exc:  # the oracle is optional for the GPU number
+            log(f"[bench] CPU baseline skipped: {exc}")
+
+    srt = sorted(per_stride)
+    line = {
+        "metric": METRIC, "value": value, "unit": "updates/s", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.description}", "grid": f"{wl.W}x{wl.H}", "C0": wl.C0,
+                   "layers": [f"{l.cin}->{l.cout} s{l.stride}{' relu' if l.relu else ''}" for l in wl.layers],
+                   "strides": "full window + warmup untimed, then the timed delta strides",
+                   "mean_pillars": float(np.mean([len(s.idx) for s in strides[1 + W:]])),
+                   "mean_active": [a / K for a in act_in]},
+        "latency_ms": {"mean": statistics.fmean(per_stride), "p50": srt[len(srt) // 2],
+                       "p99": srt[min(len(srt) - 1, int(0.99 * len(srt)))], "max": srt[-1],
+                       "over_10ms_frac": sum(1 for x in per_stride if x > 10.0) / K},
+        "alg_tflops": sum(2.0 * l.cin * l.cout * pairs[i + 1] for i, l in enumerate(wl.layers)) /
+                      (wall_ms / 1e3) / 1e12,
+        "full_recompute_ms": full_ms,
+        "speedup_vs_full_recompute": full_ms / ms_per_step,
+        "kernels": {n: {"launches": k["launches"], "avg_us": k["ms"] / k["launches"] * 1e3}
+                    for n, k in kernels.items()},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,178 @@
+/*
+ * sscater.h -- C ABI of the MI355X (gfx950) delta-scatter convolution library.
+ *
+ * The library keeps, per handle, the persistent state of a stack of 3x3
+ * convolution layers over a bird's-eye-view pillar grid and advances it one
+ * sliding-window stride at a time, touching only the cells that changed.
+ * This is the SSCATeR method (arXiv 2512.08557):
+ *
+ *   - input change map: a grid cell is "changed" when its pillar feature
+ *     vector differs from the previous window (Sec. III-B; Alg. 1, PFN part).
+ *     Here the comparison is bitwise on the stored feature vectors; a missing
+ *     pillar is an all-zero vector.
+ *   - delta scatter: each changed input site scatters
+ *     (I_curr - I_prev) x W[m,n] into the persistent output at
+ *     (i - m + floor(k/2), j - n + floor(k/2))  (Eq. 2, Sec. III-D; it fuses
+ *     the deconvolution of Eq. 1 with the convolution).  For stride 2 the
+ *     target is the downsampled site ((i-m+1)/2, (j-n+1)/2) when integral.
+ *   - change-map propagation: every output site touched by that scatter is
+ *     marked changed, including sites that the ReLU sends to zero, and for
+ *     stride 2 the downsampled sites under a changed site
+ *     (Alg. 1, backbone part; Sec. III-D, ReLU paragraph).  The next layer's
+ *     input delta at a marked site is phi(Z_new) - phi(Z_old).
+ *
+ * The result after every stride equals recomputing each layer's convolution
+ * from scratch on the whole window (abstract; Sec. V-A), up to floating-point
+ * summation order.
+ *
+ * Conventions
+ *   - grid: H rows by W columns, cell index p = r*W + c; all maps are NHWC
+ *     (a cell's channels are contiguous).
+ *   - each layer: 3x3 kernel, zero padding 1, stride 1 or 2, output extent
+ *     (n - 1)/stride + 1 per axis; weights OIHW; no bias; optional ReLU.
+ *   - dtype SSCATER_F32: fp32 features, weights, maps and accumulation.
+ *     dtype SSCATER_BF16: bf16 features, weights and layer outputs (round to
+ *     nearest even), fp32 accumulation and fp32 pre-activation maps.
+ *   - all device pointers are HIP device memory of the calling process.
+ *
+ * Streams: a handle is used with one HIP stream at a time (pass the
+ * hipStream_t as a void*, NULL = the null stream).  Calls only enqueue work on
+ * that stream and return; the exceptions, which synchronise the stream, are
+ * sscater_changed and sscater_stats.  Different handles are independent and
+ * may run concurrently on different streams.
+ *
+ * Errors: every call returns 0 or a negative SSCATER_E_* code, never throws.
+ * Device-side input faults (a cell index outside the grid or a duplicate
+ * index within one stride) set a sticky flag reported as SSCATER_E_DEVICE by
+ * the next call that finds it set after the offending stride has executed;
+ * sscater_reset clears it.
+ */
+#ifndef SSCATER_H
+#define SSCATER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SSCATER_MAX_LAYERS 32
+
+enum {
+    SSCATER_OK = 0,
+    SSCATER_E_INVALID_ARG = -1,   /* null pointer, unsupported shape, broken layer chain, bad index */
+    SSCATER_E_OUT_OF_MEMORY = -2, /* device or host allocation failed */
+    SSCATER_E_HIP = -3,           /* HIP runtime error (text via sscater_strerror) */
+    SSCATER_E_OVERFLOW = -4,      /* more pillars than max_pillars: no sampling, the stride is refused */
+    SSCATER_E_DEVICE = -5         /* sticky device-side input fault (see above) */
+};
+
+typedef enum { SSCATER_F32 = 0, SSCATER_BF16 = 1 } sscater_dtype;
+
+/* Input grid.  C0 is the pillar feature width.  max_pillars bounds the pillar
+ * count of one stride (the paper's pillar budget P with an assertion instead
+ * of random sampling, Sec. III-B). */
+typedef struct {
+    int32_t H, W, C0, max_pillars;
+    int32_t dtype; /* sscater_dtype */
+} sscater_grid;
+
+/* One convolution layer.  k must be 3 and pad 1; stride 1 or 2; relu 0 or 1.
+ * cin must equal the previous layer's cout (C0 for the first layer). */
+typedef struct {
+    int32_t cin, cout, k, stride, pad, relu;
+} sscater_layer;
+
+/* One stride's pillars (the full occupied set of the window).
+ *   idx   : device int32[count], cell indices r*W + c, unique within the call;
+ *           NULL with count == H*W selects dense mode: feats is then the whole
+ *           [H][W][C0] canvas.  NULL with count == 0 is an empty window (every
+ *           pillar vanished); feats may then be NULL too.
+ *   feats : device [count][C0] in the grid dtype (fp32, or bf16 bit patterns).
+ * Both buffers must stay valid until the stream has executed the step. */
+typedef struct {
+    const int32_t* idx;
+    const void* feats;
+    int32_t count;
+} sscater_pillars;
+
+/* Counters of the last stride and running totals since create/reset. */
+typedef struct {
+    int32_t n_layers;
+    int32_t pillars;                        /* pillar count of the last stride */
+    int64_t steps;                          /* strides since create/reset */
+    int64_t active[SSCATER_MAX_LAYERS + 1]; /* |A_l| of the last stride, l = 0..L */
+    int64_t pairs[SSCATER_MAX_LAYERS + 1];  /* (input cell, output cell) pairs of layer l = 1..L */
+    int64_t active_total[SSCATER_MAX_LAYERS + 1]; /* sums over all strides since create/reset */
+    int64_t pairs_total[SSCATER_MAX_LAYERS + 1];
+    double flops;                           /* algorithmic flops of the last stride: sum_l 2*cin*cout*pairs_l */
+    double bytes;                           /* algorithmic HBM bytes of the last stride */
+} sscater_stats_t;
+
+typedef struct sscater* sscater_t;
+
+/* Create a handle on the current HIP device.
+ *   grid, layers[n_layers] : shapes as above (1 <= n_layers <= SSCATER_MAX_LAYERS).
+ *   weights[l] : host pointer to layer l's OIHW weights [cout][cin][3][3] in the
+ *                grid dtype; copied and repacked, so the caller may free them
+ *                on return.
+ * All state (input canvas, per-layer pre-activation maps, change lists, index
+ * maps, delta buffers) is allocated here, sized for the worst case; no later
+ * call allocates.  The maps start at zero (an empty window). */
+int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
+                   const void* const* weights, sscater_t* out);
+
+/* Advance by one stride (Alg. 1): detect the changed input cells, then for
+ * each layer scatter the deltas into the persistent maps (Eq. 2) and build the
+ * next layer's change list.  The first step after create/reset is the full
+ * pass.  A stride whose input equals the previous one bit for bit changes
+ * nothing.  Asynchronous on `stream`. */
+int sscater_step(sscater_t h, const sscater_pillars* pillars, void* stream);
+
+/* Write layer `layer`'s output map into dst (device, NHWC, grid dtype):
+ * layer 0 = the input canvas, layer l >= 1 = phi(Z_l) (bf16-rounded for the
+ * bf16 dtype).  dst_bytes must be at least H_l*W_l*C_l*sizeof(dtype).
+ * Asynchronous on `stream`. */
+int sscater_read(sscater_t h, int32_t layer, void* dst, size_t dst_bytes, void* stream);
+
+/* Return to the empty window: zero the canvas and maps, forget the change
+ * lists and clear the sticky device error.  Asynchronous on `stream`. */
+int sscater_reset(sscater_t h, void* stream);
+
+/* Free everything.  The caller must make sure no work of the handle is still
+ * pending on any stream. */
+int sscater_destroy(sscater_t h);
+
+/* Test / metrics extension: the last stride's change list A_layer
+ * (0 <= layer <= L) sorted row-major into the HOST buffer dst[cap]; the list
+ * length goes to *count_host (also when it exceeds cap, in which case only cap
+ * entries are written).  Synchronises `stream`. */
+int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32_t* count_host,
+                    void* stream);
+
+/* Test / metrics extension: counters of the last stride and totals.
+ * Synchronises `stream`. */
+int sscater_stats(sscater_t h, sscater_stats_t* out, void* stream);
+
+/* Metrics extension: per-kernel timing with HIP events recorded on the
+ * step's stream around every launch of sscater_step while enabled.  Slots:
+ * 0 = input change detection (present pillars), 1 = vanished pillars,
+ * 1 + l = layer l (l = 1..L), so L + 2 slots in all.  The events add a small
+ * gap between launches; enable it only for runs that measure kernels. */
+int sscater_profile(sscater_t h, int32_t enable);
+
+/* Sum of the timed launch durations per slot (milliseconds) and the number of
+ * launches per slot since the previous read, into host arrays of n >= L + 2
+ * entries; clears the record.  Synchronises `stream`. */
+int sscater_profile_read(sscater_t h, double* ms, int64_t* launches, int32_t n, void* stream);
+
+/* Static text for an error code; for SSCATER_E_HIP the last HIP error text of
+ * the calling thread's most recent failing call. */
+const char* sscater_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSCATER_H */

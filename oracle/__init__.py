@@ -57,8 +57,15 @@ def _load():
                                             ip, ip, ip, ip, ctypes.POINTER(dp), ctypes.c_int,
                                             ctypes.POINTER(dp)]
         lib.oracle_backbone_f64.restype = ctypes.c_int
+        lib.oracle_threads.argtypes = []
+        lib.oracle_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def threads() -> int:
+    """Threads the oracle's OpenMP loops run on."""
+    return int(_load().oracle_threads())
 
 
 def _dptr(a: np.ndarray):
@@ -177,3 +184,22 @@ def canvas_bits(bits_or_values: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "bf16":
         return np.ascontiguousarray(bits_or_values, dtype=np.uint16)
     return np.ascontiguousarray(bits_or_values, dtype=np.float32).view(np.uint32)
+
+
+def pair_counts(mask: np.ndarray, stride: int) -> int:
+    """Number of (changed input cell, output cell) pairs joined by one kernel
+    tap, counted in the gather direction: for every output cell, its in-grid
+    taps that fall on a changed input cell.  This is the number of per-tap
+    contractions the scatter of Eq. 2 performs for the layer."""
+    H, W = mask.shape
+    Ho, Wo = out_extent(H, stride), out_extent(W, stride)
+    total = 0
+    ys, xs = np.arange(Ho), np.arange(Wo)
+    for m in range(3):
+        iy = stride * ys + m - 1
+        oky = (iy >= 0) & (iy < H)
+        for n in range(3):
+            ix = stride * xs + n - 1
+            okx = (ix >= 0) & (ix < W)
+            total += int(mask[np.ix_(iy[oky], ix[okx])].sum())
+    return total

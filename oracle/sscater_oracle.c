@@ -140,3 +140,15 @@ ORACLE_API int oracle_backbone_f64(const double* x0, int H0, int W0, int C0, int
     }
     return 0;
 }
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+/* Threads the oracle's parallel loops use (OpenMP's current setting). */
+ORACLE_API int oracle_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}

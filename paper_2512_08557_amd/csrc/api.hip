@@ -1,0 +1,559 @@
+// Host side of the C ABI declared in include/sscater.h: validation, worst-case
+// allocation, weight repacking and the per-stride launch sequence.
+//
+// Per stride, on the caller's stream, with no host synchronisation:
+//   1. detect (present)  : new pillars vs canvas -> A_0, packed input deltas,
+//                          canvas update, A_0 -> A_1 propagation;
+//   2. detect (vanished) : previous list minus the new list -> same outputs;
+//   3. layer l = 1..L    : contraction over A_l, Z_l update, delta epilogue,
+//                          A_l -> A_{l+1} propagation.
+// Work sizes live in device counters; the layer kernels walk their tiles from
+// the counter, so the host never waits for a count.
+//
+// Every change list is a set of cells stamped with the stride's epoch in a
+// per-grid stamp map; a map entry (epoch << 32 | row) locates the cell's row in
+// the packed delta buffer.  Bumping the epoch invalidates every list at once,
+// so no per-stride clears are needed.  The two counter sets alternate between
+// strides; the detect launch clears the set the next stride will use.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/sscater.h"
+#include "sscater_internal.h"
+
+using namespace ssc;
+
+namespace {
+
+struct LayerState {
+    sscater_layer spec{};
+    int Hin = 0, Win = 0, Hout = 0, Wout = 0;
+    float* Z = nullptr;
+    void* wpack = nullptr;
+    uint32_t* stamp = nullptr;
+    uint64_t* map = nullptr;
+    int32_t* list = nullptr;
+    void* delta = nullptr;   // packed deltas of this layer's output (nullptr for the last layer)
+};
+
+thread_local char g_hip_err[256] = "no HIP error";
+
+int hip_fail(hipError_t e) {
+    snprintf(g_hip_err, sizeof g_hip_err, "HIP error %d: %s", (int)e, hipGetErrorString(e));
+    return e == hipErrorOutOfMemory ? SSCATER_E_OUT_OF_MEMORY : SSCATER_E_HIP;
+}
+
+size_t round_up(size_t n, size_t a) { return (n + a - 1) / a * a; }
+
+int out_extent(int n, int s) { return (n + 2 - 3) / s + 1; }
+
+}  // namespace
+
+struct sscater {
+    int device = 0;
+    sscater_grid grid{};
+    int L = 0;
+    bool bf16 = false;
+    int row_bytes = 0;      // bytes of one input feature row
+    LayerState layers[SSCATER_MAX_LAYERS];
+    void* X = nullptr;
+    uint32_t* pres = nullptr;
+    uint64_t* map0 = nullptr;
+    int32_t* list0 = nullptr;
+    void* delta0 = nullptr;
+    int32_t* prev[2] = {nullptr, nullptr};
+    int prev_slot = 0;
+    int32_t prev_count = 0;
+    bool prev_dense = false;
+    int32_t* counters = nullptr;   // [2][2*(L+1)]: per set cnt[0..L], pairs[0..L]
+    long long* cum = nullptr;      // [2*(L+1)]
+    int32_t* err_host = nullptr;   // host-visible sticky error word
+    int32_t* err_dev = nullptr;
+    uint32_t epoch = 0;
+    int last_set = -1;             // counter set of the last stride, -1 after create/reset
+    long long steps = 0;
+    int32_t last_pillars = 0;
+    int layer_grid = 1024;
+    std::vector<void*> allocs;
+    // per-kernel event timing (metrics extension)
+    struct ProfRec {
+        int slot;
+        hipEvent_t a, b;
+    };
+    bool prof = false;
+    std::vector<hipEvent_t> ev_pool;
+    size_t ev_next = 0;
+    std::vector<ProfRec> prof_recs;
+
+    int ncnt() const { return 2 * (L + 1); }
+    int32_t* set_ptr(int s) { return counters + (size_t)s * ncnt(); }
+};
+
+namespace {
+
+struct DeviceGuard {
+    int prev = -1;
+    bool ok = true;
+    explicit DeviceGuard(int dev) {
+        if (hipGetDevice(&prev) != hipSuccess) { ok = false; return; }
+        if (prev != dev && hipSetDevice(dev) != hipSuccess) ok = false;
+    }
+    ~DeviceGuard() {
+        int cur = -1;
+        if (prev >= 0 && hipGetDevice(&cur) == hipSuccess && cur != prev) (void)hipSetDevice(prev);
+    }
+};
+
+int dev_alloc(sscater* h, void** p, size_t bytes) {
+    bytes = round_up(bytes < 256 ? 256 : bytes, 256);
+    hipError_t e = hipMalloc(p, bytes);
+    if (e != hipSuccess) { *p = nullptr; return hip_fail(e); }
+    h->allocs.push_back(*p);
+    e = hipMemset(*p, 0, bytes);
+    if (e != hipSuccess) return hip_fail(e);
+    return SSCATER_OK;
+}
+
+void free_all(sscater* h) {
+    for (void* p : h->allocs) (void)hipFree(p);
+    h->allocs.clear();
+    for (hipEvent_t e : h->ev_pool) (void)hipEventDestroy(e);
+    h->ev_pool.clear();
+    if (h->err_host) (void)hipHostFree(h->err_host);
+    h->err_host = nullptr;
+}
+
+bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+int check_sticky(const sscater* h) {
+    return (h->err_host && __atomic_load_n(h->err_host, __ATOMIC_ACQUIRE) != 0) ? SSCATER_E_DEVICE : SSCATER_OK;
+}
+
+hipError_t prof_event(sscater* h, hipEvent_t* out) {
+    if (h->ev_next == h->ev_pool.size()) {
+        hipEvent_t e;
+        hipError_t r = hipEventCreate(&e);
+        if (r != hipSuccess) return r;
+        h->ev_pool.push_back(e);
+    }
+    *out = h->ev_pool[h->ev_next++];
+    return hipSuccess;
+}
+
+// Launch wrapper: brackets the launch with events when profiling is enabled.
+template <class F>
+hipError_t timed_launch(sscater* h, int slot, hipStream_t s, F&& launch) {
+    if (!h->prof) return launch();
+    sscater::ProfRec r{slot, nullptr, nullptr};
+    hipError_t e = prof_event(h, &r.a);
+    if (e == hipSuccess) e = hipEventRecord(r.a, s);
+    if (e != hipSuccess) return e;
+    e = launch();
+    if (e != hipSuccess) return e;
+    e = prof_event(h, &r.b);
+    if (e == hipSuccess) e = hipEventRecord(r.b, s);
+    if (e == hipSuccess) h->prof_recs.push_back(r);
+    return e;
+}
+
+PropTarget prop_target(sscater* h, int l /* consuming layer, 1..L */, int set) {
+    PropTarget t{};
+    const LayerState& ls = h->layers[l - 1];
+    t.stride = ls.spec.stride;
+    t.Hin = ls.Hin;
+    t.Win = ls.Win;
+    t.Hout = ls.Hout;
+    t.Wout = ls.Wout;
+    t.stamp = ls.stamp;
+    t.map = ls.map;
+    t.list = ls.list;
+    t.count = h->set_ptr(set) + l;
+    t.pairs = h->set_ptr(set) + (h->L + 1) + l;
+    return t;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sscater_strerror(int code) {
+    switch (code) {
+        case SSCATER_OK: return "ok";
+        case SSCATER_E_INVALID_ARG: return "invalid argument";
+        case SSCATER_E_OUT_OF_MEMORY: return "out of memory";
+        case SSCATER_E_HIP: return g_hip_err;
+        case SSCATER_E_OVERFLOW: return "pillar count exceeds max_pillars (no sampling)";
+        case SSCATER_E_DEVICE: return "device-side input fault (cell index out of range or duplicate)";
+        default: return "unknown error";
+    }
+}
+
+int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
+                   const void* const* weights, sscater_t* out) {
+    // ---- validation: host only, before any HIP call ----
+    if (!grid || !layers || !weights || !out) return SSCATER_E_INVALID_ARG;
+    *out = nullptr;
+    if (grid->H <= 0 || grid->W <= 0 || grid->C0 <= 0 || grid->max_pillars < 0) return SSCATER_E_INVALID_ARG;
+    if (grid->dtype != SSCATER_F32 && grid->dtype != SSCATER_BF16) return SSCATER_E_INVALID_ARG;
+    if (n_layers < 1 || n_layers > SSCATER_MAX_LAYERS) return SSCATER_E_INVALID_ARG;
+    const bool bf16 = grid->dtype == SSCATER_BF16;
+    const long long cells0 = (long long)grid->H * grid->W;
+    if (cells0 > (1LL << 30)) return SSCATER_E_INVALID_ARG;
+    const int row_bytes = grid->C0 * (bf16 ? 2 : 4);
+    if (!pow2(row_bytes) || row_bytes < 16 || row_bytes > 1024) return SSCATER_E_INVALID_ARG;
+    {
+        int H = grid->H, W = grid->W, C = grid->C0;
+        for (int l = 0; l < n_layers; ++l) {
+            const sscater_layer& s = layers[l];
+            if (s.k != 3 || s.pad != 1 || (s.stride != 1 && s.stride != 2) || (s.relu != 0 && s.relu != 1))
+                return SSCATER_E_INVALID_ARG;
+            if (s.cin != C || !layer_supported(s.cin, s.cout, s.stride, bf16)) return SSCATER_E_INVALID_ARG;
+            if (!weights[l]) return SSCATER_E_INVALID_ARG;
+            H = out_extent(H, s.stride);
+            W = out_extent(W, s.stride);
+            C = s.cout;
+        }
+    }
+
+    sscater* h = new (std::nothrow) sscater();
+    if (!h) return SSCATER_E_OUT_OF_MEMORY;
+    h->grid = *grid;
+    h->L = n_layers;
+    h->bf16 = bf16;
+    h->row_bytes = row_bytes;
+    if (const char* g = getenv("SSCATER_LAYER_GRID")) {
+        const int v = atoi(g);
+        if (v >= 8 && v <= 65536) h->layer_grid = v & ~7;
+    }
+    hipError_t he = hipGetDevice(&h->device);
+    if (he != hipSuccess) {
+        delete h;
+        return hip_fail(he);
+    }
+
+    int rc = SSCATER_OK;
+    const size_t esz = bf16 ? 2 : 4;
+    const size_t cells = (size_t)cells0;
+#define SSC_TRY(expr)                 \
+    do {                              \
+        rc = (expr);                  \
+        if (rc != SSCATER_OK) goto fail; \
+    } while (0)
+    SSC_TRY(dev_alloc(h, &h->X, cells * row_bytes));
+    SSC_TRY(dev_alloc(h, (void**)&h->pres, cells * 4));
+    SSC_TRY(dev_alloc(h, (void**)&h->map0, cells * 8));
+    SSC_TRY(dev_alloc(h, (void**)&h->list0, cells * 4));
+    // A_0 holds at most every cell (dense mode); fp32 rows or bf16 [new | old] pairs
+    SSC_TRY(dev_alloc(h, &h->delta0, cells * (size_t)(bf16 ? 2 * row_bytes : row_bytes)));
+    SSC_TRY(dev_alloc(h, (void**)&h->prev[0], (size_t)grid->max_pillars * 4));
+    SSC_TRY(dev_alloc(h, (void**)&h->prev[1], (size_t)grid->max_pillars * 4));
+    SSC_TRY(dev_alloc(h, (void**)&h->counters, (size_t)2 * h->ncnt() * 4));
+    SSC_TRY(dev_alloc(h, (void**)&h->cum, (size_t)h->ncnt() * 8));
+    {
+        int H = grid->H, W = grid->W;
+        for (int l = 0; l < n_layers; ++l) {
+            LayerState& ls = h->layers[l];
+            ls.spec = layers[l];
+            ls.Hin = H;
+            ls.Win = W;
+            ls.Hout = out_extent(H, ls.spec.stride);
+            ls.Wout = out_extent(W, ls.spec.stride);
+            const size_t oc = (size_t)ls.Hout * ls.Wout;
+            SSC_TRY(dev_alloc(h, (void**)&ls.Z, oc * ls.spec.cout * 4));
+            SSC_TRY(dev_alloc(h, (void**)&ls.stamp, oc * 4));
+            SSC_TRY(dev_alloc(h, (void**)&ls.map, oc * 8));
+            SSC_TRY(dev_alloc(h, (void**)&ls.list, oc * 4));
+            if (l + 1 < n_layers) SSC_TRY(dev_alloc(h, &ls.delta, oc * ls.spec.cout * 4));
+            const size_t wn = wpack_elems(ls.spec.cin, ls.spec.cout, bf16);
+            std::vector<unsigned char> packed(wn * esz);
+            pack_weights(weights[l], ls.spec.cin, ls.spec.cout, bf16, packed.data());
+            SSC_TRY(dev_alloc(h, &ls.wpack, wn * esz));
+            he = hipMemcpy(ls.wpack, packed.data(), wn * esz, hipMemcpyHostToDevice);
+            if (he != hipSuccess) { rc = hip_fail(he); goto fail; }
+            H = ls.Hout;
+            W = ls.Wout;
+        }
+    }
+    he = hipHostMalloc((void**)&h->err_host, 256, hipHostMallocMapped | hipHostMallocCoherent);
+    if (he != hipSuccess) { h->err_host = nullptr; rc = hip_fail(he); goto fail; }
+    *h->err_host = 0;
+    he = hipHostGetDevicePointer((void**)&h->err_dev, h->err_host, 0);
+    if (he != hipSuccess) { rc = hip_fail(he); goto fail; }
+    he = hipDeviceSynchronize();
+    if (he != hipSuccess) { rc = hip_fail(he); goto fail; }
+#undef SSC_TRY
+    h->epoch = 0;
+    *out = h;
+    return SSCATER_OK;
+fail:
+    free_all(h);
+    delete h;
+    return rc;
+}
+
+int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
+    if (!h || !pl) return SSCATER_E_INVALID_ARG;
+    if (int rc = check_sticky(h)) return rc;
+    const long long cells = (long long)h->grid.H * h->grid.W;
+    // NULL idx with count == H*W is dense mode; NULL idx with count 0 is an empty stride
+    const bool dense = pl->idx == nullptr && pl->count != 0;
+    if (dense) {
+        if (pl->count != cells || !pl->feats) return SSCATER_E_INVALID_ARG;
+    } else {
+        if (pl->count < 0) return SSCATER_E_INVALID_ARG;
+        if (pl->count > h->grid.max_pillars) return SSCATER_E_OVERFLOW;
+        if (pl->count > 0 && !pl->feats) return SSCATER_E_INVALID_ARG;
+    }
+    DeviceGuard dg(h->device);
+    if (!dg.ok) return hip_fail(hipGetLastError());
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    const uint32_t epoch = ++h->epoch;
+    const int set = (int)(epoch & 1u);
+    int32_t* cnt = h->set_ptr(set);
+    const int cur_slot = h->prev_slot ^ 1;
+
+    DetectArgs d{};
+    d.idx = pl->idx;
+    d.feats = pl->feats;
+    d.count = pl->count;
+    d.prev = nullptr;
+    d.prev_out = dense ? nullptr : h->prev[cur_slot];
+    d.X = h->X;
+    d.pres = h->pres;
+    d.map0 = h->map0;
+    d.list0 = h->list0;
+    d.count0 = cnt;
+    d.delta0 = h->delta0;
+    d.zero_ptr = h->set_ptr(set ^ 1);
+    d.zero_n = h->ncnt();
+    d.HW = (int32_t)cells;
+    d.epoch = epoch;
+    d.err = h->err_dev;
+    d.next = prop_target(h, 1, set);
+    hipError_t e = timed_launch(h, 0, s, [&] { return launch_detect_present(d, h->row_bytes, h->bf16, s); });
+    if (e != hipSuccess) return hip_fail(e);
+
+    if (!dense && (h->prev_dense || h->prev_count > 0)) {
+        DetectArgs v = d;
+        v.prev = h->prev_dense ? nullptr : h->prev[h->prev_slot];
+        v.count = h->prev_dense ? (int32_t)cells : h->prev_count;
+        v.prev_out = nullptr;
+        v.zero_ptr = nullptr;
+        v.zero_n = 0;
+        e = timed_launch(h, 1, s, [&] { return launch_detect_vanished(v, h->row_bytes, h->bf16, s); });
+        if (e != hipSuccess) return hip_fail(e);
+    }
+
+    for (int l = 1; l <= h->L; ++l) {
+        LayerState& ls = h->layers[l - 1];
+        LayerArgs a{};
+        a.list = ls.list;
+        a.count = cnt + l;
+        a.map_in = l == 1 ? h->map0 : h->layers[l - 2].map;
+        a.delta_in = l == 1 ? h->delta0 : h->layers[l - 2].delta;
+        a.wpack = ls.wpack;
+        a.Z = ls.Z;
+        a.delta_out = l < h->L ? ls.delta : nullptr;
+        a.Hin = ls.Hin;
+        a.Win = ls.Win;
+        a.Hout = ls.Hout;
+        a.Wout = ls.Wout;
+        a.relu = ls.spec.relu;
+        a.epoch = epoch;
+        a.has_next = l < h->L;
+        if (a.has_next) a.next = prop_target(h, l + 1, set);
+        if (l == h->L) {
+            a.cum_src = cnt;
+            a.cum_dst = h->cum;
+            a.n_cum = h->ncnt();
+        }
+        e = timed_launch(h, 1 + l, s, [&] {
+            return launch_layer(a, ls.spec.cin, ls.spec.cout, ls.spec.stride, h->bf16, h->layer_grid, s);
+        });
+        if (e != hipSuccess) return hip_fail(e);
+    }
+
+    if (!dense) {
+        h->prev_slot = cur_slot;
+        h->prev_count = pl->count;
+        h->prev_dense = false;
+    } else {
+        h->prev_count = 0;
+        h->prev_dense = true;
+    }
+    h->last_set = set;
+    h->steps += 1;
+    h->last_pillars = pl->count;
+    return SSCATER_OK;
+}
+
+int sscater_read(sscater_t h, int32_t layer, void* dst, size_t dst_bytes, void* stream) {
+    if (!h || !dst || layer < 0 || layer > h->L) return SSCATER_E_INVALID_ARG;
+    if (int rc = check_sticky(h)) return rc;
+    DeviceGuard dg(h->device);
+    if (!dg.ok) return hip_fail(hipGetLastError());
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const size_t esz = h->bf16 ? 2 : 4;
+    if (layer == 0) {
+        const size_t need = (size_t)h->grid.H * h->grid.W * h->row_bytes;
+        if (dst_bytes < need) return SSCATER_E_INVALID_ARG;
+        hipError_t e = hipMemcpyAsync(dst, h->X, need, hipMemcpyDeviceToDevice, s);
+        return e == hipSuccess ? SSCATER_OK : hip_fail(e);
+    }
+    const LayerState& ls = h->layers[layer - 1];
+    const long long n = (long long)ls.Hout * ls.Wout * ls.spec.cout;
+    if (dst_bytes < (size_t)n * esz) return SSCATER_E_INVALID_ARG;
+    hipError_t e = launch_read(ls.Z, dst, n, ls.spec.relu, h->bf16, s);
+    return e == hipSuccess ? SSCATER_OK : hip_fail(e);
+}
+
+int sscater_reset(sscater_t h, void* stream) {
+    if (!h) return SSCATER_E_INVALID_ARG;
+    DeviceGuard dg(h->device);
+    if (!dg.ok) return hip_fail(hipGetLastError());
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // The library drains the stream before clearing the host-visible error
+    // word, so a fault of a stride still in flight cannot survive the reset.
+    hipError_t e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e);
+    const size_t cells = (size_t)h->grid.H * h->grid.W;
+    e = launch_fill_zero(h->X, round_up(cells * h->row_bytes, 256), s);
+    for (int l = 0; l < h->L && e == hipSuccess; ++l) {
+        const LayerState& ls = h->layers[l];
+        e = launch_fill_zero(ls.Z, round_up((size_t)ls.Hout * ls.Wout * ls.spec.cout * 4, 256), s);
+    }
+    if (e == hipSuccess) e = launch_fill_zero(h->counters, round_up((size_t)2 * h->ncnt() * 4, 256), s);
+    if (e == hipSuccess) e = launch_fill_zero(h->cum, round_up((size_t)h->ncnt() * 8, 256), s);
+    if (e != hipSuccess) return hip_fail(e);
+    ++h->epoch;   // every stamp and index map becomes stale
+    h->prev_count = 0;
+    h->prev_dense = false;
+    h->last_set = -1;
+    h->steps = 0;
+    h->last_pillars = 0;
+    __atomic_store_n(h->err_host, 0, __ATOMIC_RELEASE);
+    return SSCATER_OK;
+}
+
+int sscater_destroy(sscater_t h) {
+    if (!h) return SSCATER_E_INVALID_ARG;
+    {
+        DeviceGuard dg(h->device);
+        free_all(h);
+    }
+    delete h;
+    return SSCATER_OK;
+}
+
+int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32_t* count_host, void* stream) {
+    if (!h || !count_host || layer < 0 || layer > h->L || cap < 0 || (cap > 0 && !dst))
+        return SSCATER_E_INVALID_ARG;
+    DeviceGuard dg(h->device);
+    if (!dg.ok) return hip_fail(hipGetLastError());
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e);
+    if (int rc = check_sticky(h)) return rc;
+    if (h->last_set < 0) {
+        *count_host = 0;
+        return SSCATER_OK;
+    }
+    int32_t n = 0;
+    e = hipMemcpy(&n, h->set_ptr(h->last_set) + layer, 4, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e);
+    *count_host = n;
+    if (n == 0) return SSCATER_OK;
+    std::vector<int32_t> buf((size_t)n);
+    const int32_t* src = layer == 0 ? h->list0 : h->layers[layer - 1].list;
+    e = hipMemcpy(buf.data(), src, (size_t)n * 4, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e);
+    std::sort(buf.begin(), buf.end());
+    std::memcpy(dst, buf.data(), (size_t)std::min(n, cap) * 4);
+    return SSCATER_OK;
+}
+
+int sscater_stats(sscater_t h, sscater_stats_t* out, void* stream) {
+    if (!h || !out) return SSCATER_E_INVALID_ARG;
+    DeviceGuard dg(h->device);
+    if (!dg.ok) return hip_fail(hipGetLastError());
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e);
+    std::memset(out, 0, sizeof *out);
+    const int L = h->L;
+    out->n_layers = L;
+    out->steps = h->steps;
+    out->pillars = h->last_pillars;
+    std::vector<int32_t> c((size_t)h->ncnt(), 0);
+    std::vector<long long> t((size_t)h->ncnt(), 0);
+    if (h->last_set >= 0) {
+        e = hipMemcpy(c.data(), h->set_ptr(h->last_set), c.size() * 4, hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(e);
+    }
+    e = hipMemcpy(t.data(), h->cum, t.size() * 8, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e);
+    for (int l = 0; l <= L; ++l) {
+        out->active[l] = c[l];
+        out->pairs[l] = c[L + 1 + l];
+        out->active_total[l] = t[l];
+        out->pairs_total[l] = t[L + 1 + l];
+    }
+    // algorithmic flops and HBM bytes of the last stride (the method's own work)
+    const double e_in = h->bf16 ? 2.0 : 4.0;        // stored feature element
+    const double e_d = 4.0;                          // packed delta element (fp32, or bf16 pair)
+    const double P = (double)h->last_pillars, C0 = (double)h->grid.C0;
+    double flops = 0.0;
+    double bytes = P * (4.0 + C0 * e_in)             // new pillar list
+                   + P * C0 * e_in                   // canvas compare gather
+                   + (double)c[0] * C0 * (e_in + e_d);  // canvas write + packed input deltas
+    for (int l = 1; l <= L; ++l) {
+        const sscater_layer& sp = h->layers[l - 1].spec;
+        const double a_in = c[l - 1], a_out = c[l], pairs = c[L + 1 + l];
+        flops += 2.0 * sp.cin * sp.cout * pairs;
+        bytes += a_in * sp.cin * e_d                 // packed input deltas
+                 + a_out * sp.cout * 8.0             // Z read + write
+                 + (l < L ? a_out * sp.cout * e_d : 0.0)   // emitted deltas
+                 + 9.0 * sp.cin * sp.cout * e_in     // weights
+                 + 12.0 * (a_in + a_out);            // lists and index maps
+    }
+    out->flops = flops;
+    out->bytes = bytes;
+    return check_sticky(h);
+}
+
+int sscater_profile(sscater_t h, int32_t enable) {
+    if (!h) return SSCATER_E_INVALID_ARG;
+    h->prof = enable != 0;
+    return SSCATER_OK;
+}
+
+int sscater_profile_read(sscater_t h, double* ms, int64_t* launches, int32_t n, void* stream) {
+    if (!h || !ms || !launches || n < h->L + 2) return SSCATER_E_INVALID_ARG;
+    DeviceGuard dg(h->device);
+    if (!dg.ok) return hip_fail(hipGetLastError());
+    hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e);
+    for (int i = 0; i < n; ++i) {
+        ms[i] = 0.0;
+        launches[i] = 0;
+    }
+    for (const auto& r : h->prof_recs) {
+        float t = 0.f;
+        e = hipEventElapsedTime(&t, r.a, r.b);
+        if (e != hipSuccess) return hip_fail(e);
+        ms[r.slot] += t;
+        launches[r.slot] += 1;
+    }
+    h->prof_recs.clear();
+    h->ev_next = 0;
+    return SSCATER_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,131 @@
+// Changed-cell detector on the input canvas, with stream compaction into the
+// input change list A_0, packing of the input deltas in A_0 order, canvas
+// update and propagation of A_0 to the first layer's change list.
+//
+// A cell is changed when its stored feature vector differs bit for bit from
+// the canvas (a pillar whose points changed: Sec. III-B and Alg. 1, PFN part).
+// Two passes per stride:
+//   present  : every pillar of the new list is compared with the canvas;
+//   vanished : every cell of the previous list that is absent from the new
+//              list is compared with zero (its pillar disappeared).
+// The second pass needs the presence stamps of the whole first pass, so it is
+// a separate launch.
+//
+// Layout: LANES = row_bytes / 16 lanes share one feature row, each lane moving
+// 16 bytes, so a 64-channel fp32 row (256 B) is one fully coalesced 16-lane
+// access.  Delta rows: fp32 new - old, or for bf16 the pair [new | old] that
+// the layer kernels contract with [W | -W] (exact products, no delta rounding).
+#include "device_common.h"
+
+namespace ssc {
+
+template <int ROWB, bool BF16, bool VANISH>
+__global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
+    constexpr int G = ROWB / 16;   // lanes per feature row
+    constexpr int PPW = 64 / G;    // rows per wavefront pass
+    const int lane = lane_id();
+    const int sub = lane % G;
+    const int gbase = lane - sub;
+
+    if (!VANISH && a.zero_ptr && blockIdx.x == 0)
+        for (int i = threadIdx.x; i < a.zero_n; i += blockDim.x) a.zero_ptr[i] = 0;
+
+    const int wave = (int)((blockIdx.x * blockDim.x + threadIdx.x) >> 6);
+    const int nwaves = (int)((gridDim.x * blockDim.x) >> 6);
+    for (int base = wave * PPW; base < a.count; base += nwaves * PPW) {
+        const int i = base + lane / G;
+        bool act = i < a.count;
+        int p = -1;
+        if (act) {
+            if (VANISH) p = a.prev ? a.prev[i] : i;
+            else p = a.idx ? a.idx[i] : i;
+            if (p < 0 || p >= a.HW) {
+                if (!VANISH && sub == 0) flag_error(a.err, ERR_INDEX_RANGE);
+                act = false;
+            }
+        }
+        // presence stamps: a pillar marks its cell present for this stride;
+        // a second pillar on the same cell is an input fault.
+        uint32_t st = 0;
+        if (act && sub == 0) st = VANISH ? a.pres[p] : atomicExch(&a.pres[p], a.epoch);
+        st = __shfl(st, gbase);
+        if (act && st == a.epoch) {
+            if (!VANISH && sub == 0) flag_error(a.err, ERR_DUPLICATE);
+            act = false;
+        }
+        uint4 nv = make_uint4(0u, 0u, 0u, 0u), ov = make_uint4(0u, 0u, 0u, 0u);
+        char* xrow = static_cast<char*>(a.X) + (size_t)(act ? p : 0) * ROWB + sub * 16;
+        if (act) {
+            ov = *reinterpret_cast<const uint4*>(xrow);
+            if (!VANISH)
+                nv = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.feats) + (size_t)i * ROWB +
+                                                     sub * 16);
+        }
+        const bool d = act && (nv.x != ov.x || nv.y != ov.y || nv.z != ov.z || nv.w != ov.w);
+        const unsigned long long bal = __ballot(d);
+        const unsigned long long gm = (G == 64 ? ~0ull : ((1ull << G) - 1ull)) << gbase;
+        const bool gd = (bal & gm) != 0ull;
+        int row = wave_append(a.count0, gd && sub == 0);
+        row = __shfl(row, gbase);
+        if (gd) {
+            if (BF16) {
+                char* drow = static_cast<char*>(a.delta0) + (size_t)row * (2 * ROWB);
+                *reinterpret_cast<uint4*>(drow + sub * 16) = nv;
+                *reinterpret_cast<uint4*>(drow + ROWB + sub * 16) = ov;
+            } else {
+                f4v dn;
+                dn.x = __uint_as_float(nv.x) - __uint_as_float(ov.x);
+                dn.y = __uint_as_float(nv.y) - __uint_as_float(ov.y);
+                dn.z = __uint_as_float(nv.z) - __uint_as_float(ov.z);
+                dn.w = __uint_as_float(nv.w) - __uint_as_float(ov.w);
+                *reinterpret_cast<f4v*>(static_cast<char*>(a.delta0) + (size_t)row * ROWB + sub * 16) = dn;
+            }
+            *reinterpret_cast<uint4*>(xrow) = nv;
+            if (sub == 0) {
+                a.list0[row] = p;
+                a.map0[p] = ((uint64_t)a.epoch << 32) | (uint32_t)row;
+            }
+        }
+        if (!VANISH && a.prev_out && sub == 0 && i < a.count) a.prev_out[i] = act ? p : -1;
+        propagate_cells<G>(a.next, gd ? p : -1, sub, a.epoch);
+    }
+}
+
+template <bool VANISH>
+static hipError_t launch_detect(const DetectArgs& a, int row_bytes, bool bf16, hipStream_t s) {
+    const int G = row_bytes / 16;
+    const int ppw = 64 / G;
+    long long waves = ((long long)a.count + ppw - 1) / ppw;
+    long long blocks = (waves + 3) / 4;
+    if (blocks < 1) blocks = 1;
+    if (blocks > 4096) blocks = 4096;
+    dim3 grid((unsigned)blocks), block(256);
+#define SSC_DETECT_CASE(RB)                                                                      \
+    case RB:                                                                                     \
+        if (bf16) hipLaunchKernelGGL((detect_kernel<RB, true, VANISH>), grid, block, 0, s, a);   \
+        else hipLaunchKernelGGL((detect_kernel<RB, false, VANISH>), grid, block, 0, s, a);       \
+        break;
+    switch (row_bytes) {
+        SSC_DETECT_CASE(16)
+        SSC_DETECT_CASE(32)
+        SSC_DETECT_CASE(64)
+        SSC_DETECT_CASE(128)
+        SSC_DETECT_CASE(256)
+        SSC_DETECT_CASE(512)
+        SSC_DETECT_CASE(1024)
+        default:
+            return hipErrorInvalidValue;
+    }
+#undef SSC_DETECT_CASE
+    return hipGetLastError();
+}
+
+hipError_t launch_detect_present(const DetectArgs& a, int row_bytes, bool bf16, hipStream_t s) {
+    return launch_detect<false>(a, row_bytes, bf16, s);
+}
+
+hipError_t launch_detect_vanished(const DetectArgs& a, int row_bytes, bool bf16, hipStream_t s) {
+    return launch_detect<true>(a, row_bytes, bf16, s);
+}
+
+}  // namespace ssc

@@ -1,0 +1,89 @@
+// Device helpers shared by the kernels: wavefront-aggregated list appends and
+// the structural change-list propagation rule.
+#pragma once
+
+#include "sscater_internal.h"
+
+namespace ssc {
+
+typedef float f4v __attribute__((ext_vector_type(4)));
+typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63u); }
+
+// Append one entry per lane whose `pred` is set to a device list whose length
+// is *counter: one atomic per wavefront, positions in lane order.  Must be
+// reached by every lane of the wavefront.  Returns the lane's slot or -1.
+__device__ __forceinline__ int wave_append(int32_t* counter, bool pred) {
+    const unsigned long long m = __ballot(pred);
+    if (m == 0ull) return -1;
+    const int lane = lane_id();
+    const int leader = __ffsll((long long)m) - 1;
+    int base = 0;
+    if (lane == leader) base = atomicAdd(counter, (int)__popcll(m));
+    base = __shfl(base, leader);
+    const int rank = (int)__popcll(m & ((1ull << lane) - 1ull));
+    return pred ? base + rank : -1;
+}
+
+__device__ __forceinline__ int wave_sum(int v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+// Structural propagation of changed cells to the next layer's list.
+// Cell `cell` of the grid (t.Hin x t.Win) (or -1 for none) feeds output
+// ((i - m + 1)/s, (j - n + 1)/s) through tap (m, n) when both quotients are
+// integral and inside (t.Hout x t.Wout): the scatter target of Eq. 2
+// generalised to stride s, and the downsampling rule of Alg. 1 for s = 2.
+// Each cell is handled by G lanes that share the 9 tap slots (slot = sub +
+// it*G).  Every touched output cell is stamped with `epoch`; the first lane
+// to stamp it appends it to t.list and records its position in t.map.  The
+// number of (cell, tap) pairs with an in-grid target is added to *t.pairs.
+// Must be reached by every lane of the wavefront.
+template <int G>
+__device__ __forceinline__ void propagate_cells(const PropTarget& t, int cell, int sub, uint32_t epoch) {
+    constexpr int ITERS = (9 + G - 1) / G;
+    int npairs = 0;
+#pragma unroll
+    for (int it = 0; it < ITERS; ++it) {
+        const int k = sub + it * G;
+        int q = -1;
+        if (cell >= 0 && k < 9) {
+            const int i = cell / t.Win, j = cell - (cell / t.Win) * t.Win;
+            const int m = k / 3, n = k - 3 * (k / 3);
+            int rn = i - m + 1, cn = j - n + 1;     // >= -1
+            bool ok = true;
+            if (t.stride == 2) {
+                ok = ((rn | cn) & 1) == 0;
+                rn >>= 1;
+                cn >>= 1;
+            }
+            if (ok && rn >= 0 && rn < t.Hout && cn >= 0 && cn < t.Wout) q = rn * t.Wout + cn;
+        }
+        npairs += (q >= 0) ? 1 : 0;
+        bool own = false;
+        if (q >= 0) own = atomicMax(&t.stamp[q], epoch) < epoch;
+        const int r = wave_append(t.count, own);
+        if (own) {
+            t.list[r] = q;
+            t.map[q] = ((uint64_t)epoch << 32) | (uint32_t)r;
+        }
+    }
+    npairs = wave_sum(npairs);
+    if (lane_id() == 0 && npairs) atomicAdd(t.pairs, npairs);
+}
+
+// fp32 -> bf16 bits, round to nearest even (finite values).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+__device__ __forceinline__ void flag_error(int32_t* err, int bit) {
+    *(volatile int32_t*)err = bit;
+}
+
+}  // namespace ssc

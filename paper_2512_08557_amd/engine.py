@@ -1,0 +1,215 @@
+"""ctypes binding of libsscater.so (argument marshalling only).
+
+Every step of the hot path runs in the library's HIP kernels; this module
+only converts Python/torch arguments into the C ABI of include/sscater.h:
+device pointers come from ``tensor.data_ptr()`` and the HIP stream from
+``torch.cuda.current_stream().cuda_stream``.  There is no fallback: if the
+library is missing, importing the binding raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsscater.so")
+
+MAX_LAYERS = 32
+OK, E_INVALID_ARG, E_OUT_OF_MEMORY, E_HIP, E_OVERFLOW, E_DEVICE = 0, -1, -2, -3, -4, -5
+F32, BF16 = 0, 1
+
+# every function declared in include/sscater.h
+EXPORTS = ("sscater_create", "sscater_step", "sscater_read", "sscater_reset", "sscater_destroy",
+           "sscater_changed", "sscater_stats", "sscater_profile", "sscater_profile_read", "sscater_strerror")
+
+
+class Grid(ctypes.Structure):
+    _fields_ = [("H", ctypes.c_int32), ("W", ctypes.c_int32), ("C0", ctypes.c_int32),
+                ("max_pillars", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [("cin", ctypes.c_int32), ("cout", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("stride", ctypes.c_int32), ("pad", ctypes.c_int32), ("relu", ctypes.c_int32)]
+
+
+class Pillars(ctypes.Structure):
+    _fields_ = [("idx", ctypes.c_void_p), ("feats", ctypes.c_void_p), ("count", ctypes.c_int32)]
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("pillars", ctypes.c_int32), ("steps", ctypes.c_int64),
+                ("active", ctypes.c_int64 * (MAX_LAYERS + 1)), ("pairs", ctypes.c_int64 * (MAX_LAYERS + 1)),
+                ("active_total", ctypes.c_int64 * (MAX_LAYERS + 1)),
+                ("pairs_total", ctypes.c_int64 * (MAX_LAYERS + 1)),
+                ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
+
+
+class SscaterError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {lib().sscater_strerror(code).decode()} ({code})")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"HIP library not built: {LIB_PATH} (run __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32 = ctypes.c_void_p, ctypes.c_int32
+        L.sscater_create.argtypes = [ctypes.POINTER(Grid), ctypes.POINTER(Layer), i32,
+                                     ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(vp)]
+        L.sscater_step.argtypes = [vp, ctypes.POINTER(Pillars), vp]
+        L.sscater_read.argtypes = [vp, i32, vp, ctypes.c_size_t, vp]
+        L.sscater_reset.argtypes = [vp, vp]
+        L.sscater_destroy.argtypes = [vp]
+        L.sscater_changed.argtypes = [vp, i32, ctypes.POINTER(i32), i32, ctypes.POINTER(i32), vp]
+        L.sscater_stats.argtypes = [vp, ctypes.POINTER(Stats), vp]
+        L.sscater_profile.argtypes = [vp, i32]
+        L.sscater_profile_read.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), i32,
+                                           vp]
+        L.sscater_strerror.argtypes = [ctypes.c_int]
+        L.sscater_strerror.restype = ctypes.c_char_p
+        for f in EXPORTS[:-1]:
+            getattr(L, f).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(rc: int, where: str) -> None:
+    if rc != OK:
+        raise SscaterError(rc, where)
+
+
+def out_extent(n: int, stride: int) -> int:
+    return (n - 1) // stride + 1
+
+
+def weights_to_dtype_bytes(w: np.ndarray, dtype: str) -> np.ndarray:
+    """OIHW weights as the grid dtype's bytes: float32, or the bf16 bit
+    patterns of values that are exactly representable in bf16."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    if dtype == "f32":
+        return w
+    u = w.view(np.uint32)
+    if np.any(u & 0xFFFF):
+        raise ValueError("bf16 weights must be exactly representable in bfloat16")
+    return np.ascontiguousarray((u >> 16).astype(np.uint16))
+
+
+class Engine:
+    """One handle of the delta-scatter backbone state (one sensor stream)."""
+
+    def __init__(self, H: int, W: int, C0: int, layers: Sequence[Tuple[int, int, int, bool]],
+                 weights: Sequence[np.ndarray], dtype: str = "f32", max_pillars: int = 16000):
+        import torch  # device memory and streams only
+        self._torch = torch
+        self.H, self.W, self.C0 = H, W, C0
+        self.dtype = dtype
+        self.layers = [tuple(l) for l in layers]
+        self.shapes = [(H, W, C0)]
+        h, w = H, W
+        for (cin, cout, s, _r) in self.layers:
+            h, w = out_extent(h, s), out_extent(w, s)
+            self.shapes.append((h, w, cout))
+        grid = Grid(H, W, C0, max_pillars, BF16 if dtype == "bf16" else F32)
+        n = len(self.layers)
+        larr = (Layer * n)(*[Layer(ci, co, 3, s, 1, int(bool(r))) for (ci, co, s, r) in self.layers])
+        self._wbufs = [weights_to_dtype_bytes(wt, dtype) for wt in weights]
+        if len(self._wbufs) != n:
+            raise ValueError("one weight tensor per layer")
+        wptrs = (ctypes.c_void_p * n)(*[b.ctypes.data for b in self._wbufs])
+        handle = ctypes.c_void_p()
+        _check(lib().sscater_create(ctypes.byref(grid), larr, n, wptrs, ctypes.byref(handle)), "sscater_create")
+        self._h = handle
+        self._wbufs = None   # copied by the library
+
+    # -- helpers ---------------------------------------------------------------
+    def _stream(self, stream=None) -> ctypes.c_void_p:
+        t = self._torch
+        s = stream if stream is not None else t.cuda.current_stream()
+        return ctypes.c_void_p(s.cuda_stream)
+
+    @property
+    def torch_dtype(self):
+        return self._torch.float32 if self.dtype == "f32" else self._torch.bfloat16
+
+    # -- C ABI calls -------------------------------------------------------------
+    def step(self, idx, feats, stream=None) -> None:
+        """idx: int32 cuda tensor [P] (or None for a dense [H, W, C0] canvas);
+        feats: cuda tensor [P, C0] of the grid dtype (float32, or bf16 bits as
+        int16/uint16/bfloat16)."""
+        if idx is not None:
+            if idx.dtype != self._torch.int32 or not idx.is_cuda or not idx.is_contiguous():
+                raise ValueError("idx must be a contiguous int32 cuda tensor")
+            count = idx.numel()
+        else:
+            count = self.H * self.W
+        if count and (not feats.is_cuda or not feats.is_contiguous() or feats.element_size() !=
+                      (4 if self.dtype == "f32" else 2) or feats.numel() != count * self.C0):
+            raise ValueError("feats must be a contiguous cuda tensor [count, C0] of the grid dtype")
+        p = Pillars(idx.data_ptr() if idx is not None else None, feats.data_ptr() if count else None, count)
+        _check(lib().sscater_step(self._h, ctypes.byref(p), self._stream(stream)), "sscater_step")
+
+    def read(self, layer: int, out=None, stream=None):
+        h, w, c = self.shapes[layer]
+        if out is None:
+            out = self._torch.empty((h, w, c), dtype=self.torch_dtype, device="cuda")
+        _check(lib().sscater_read(self._h, layer, ctypes.c_void_p(out.data_ptr()),
+                                  out.numel() * out.element_size(), self._stream(stream)), "sscater_read")
+        return out
+
+    def reset(self, stream=None) -> None:
+        _check(lib().sscater_reset(self._h, self._stream(stream)), "sscater_reset")
+
+    def changed(self, layer: int, stream=None) -> np.ndarray:
+        h, w, _ = self.shapes[layer]
+        cap = h * w
+        buf = np.empty(cap, dtype=np.int32)
+        cnt = ctypes.c_int32(0)
+        _check(lib().sscater_changed(self._h, layer, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), cap,
+                                     ctypes.byref(cnt), self._stream(stream)), "sscater_changed")
+        return buf[:cnt.value].copy()
+
+    def stats(self, stream=None) -> Dict:
+        st = Stats()
+        _check(lib().sscater_stats(self._h, ctypes.byref(st), self._stream(stream)), "sscater_stats")
+        L = st.n_layers
+        return dict(steps=st.steps, pillars=st.pillars, active=list(st.active[:L + 1]),
+                    pairs=list(st.pairs[:L + 1]), active_total=list(st.active_total[:L + 1]),
+                    pairs_total=list(st.pairs_total[:L + 1]), flops=st.flops, bytes=st.bytes)
+
+    def profile(self, enable: bool) -> None:
+        _check(lib().sscater_profile(self._h, int(bool(enable))), "sscater_profile")
+
+    def profile_read(self, stream=None):
+        """(ms per slot, launches per slot); slot 0 detect, 1 vanished, 1+l layer l."""
+        n = len(self.layers) + 2
+        ms = (ctypes.c_double * n)()
+        cnt = (ctypes.c_int64 * n)()
+        _check(lib().sscater_profile_read(self._h, ms, cnt, n, self._stream(stream)), "sscater_profile_read")
+        return list(ms), list(cnt)
+
+    def close(self) -> None:
+        if getattr(self, "_h", None):
+            _check(lib().sscater_destroy(self._h), "sscater_destroy")
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

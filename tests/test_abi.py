@@ -1,0 +1,104 @@
+"""C-ABI surface checks that need no GPU: every symbol declared in
+include/sscater.h is exported by the built library, and host-side argument
+validation rejects bad calls before any HIP work."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2512_08557_amd as ssc
+from paper_2512_08557_amd import engine as E
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    txt = open(os.path.join(ROOT, "include", "sscater.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(sscater_[a-z_]+)\s*\(", txt)))
+
+
+def test_header_declares_the_binding_surface():
+    assert _declared() == sorted(E.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(ssc.LIB_PATH)
+    for name in _declared():
+        assert hasattr(lib, name), name
+
+
+def test_strerror_texts():
+    lib = ssc.lib()
+    for code in (0, -1, -2, -3, -4, -5, -99):
+        assert isinstance(lib.sscater_strerror(code), bytes)
+    assert b"max_pillars" in lib.sscater_strerror(ssc.E_OVERFLOW)
+
+
+def _create(grid, layers, weights=True):
+    lib = ssc.lib()
+    n = len(layers)
+    larr = (E.Layer * max(n, 1))(*layers) if n else None
+    bufs = [np.zeros((l.cout, l.cin, 3, 3), np.float32) for l in layers]
+    wp = (ctypes.c_void_p * max(n, 1))(*[b.ctypes.data for b in bufs]) if weights else None
+    h = ctypes.c_void_p()
+    return lib.sscater_create(ctypes.byref(grid) if grid is not None else None, larr, n, wp, ctypes.byref(h))
+
+
+@pytest.mark.parametrize("case", [
+    "null_grid", "no_layers", "k5", "pad0", "stride3", "chain", "unsupported_cout", "bad_c0", "bad_dtype",
+    "relu2", "too_many_layers", "huge_grid", "null_weights"])
+def test_create_rejects_invalid_arguments(case):
+    g = E.Grid(32, 32, 64, 100, E.F32)
+    L = [E.Layer(64, 64, 3, 2, 1, 1), E.Layer(64, 64, 3, 1, 1, 1)]
+    weights = True
+    if case == "null_grid":
+        g = None
+    elif case == "no_layers":
+        L = []
+    elif case == "k5":
+        L[0].k = 5
+    elif case == "pad0":
+        L[1].pad = 0
+    elif case == "stride3":
+        L[0].stride = 3
+    elif case == "chain":
+        L[1].cin = 32
+    elif case == "unsupported_cout":
+        L[1].cout = 24
+    elif case == "bad_c0":
+        g.C0 = 48
+    elif case == "bad_dtype":
+        g.dtype = 7
+    elif case == "relu2":
+        L[0].relu = 2
+    elif case == "too_many_layers":
+        L = [E.Layer(64, 64, 3, 1, 1, 1)] * 33
+    elif case == "huge_grid":
+        g.H, g.W = 1 << 16, 1 << 16
+    elif case == "null_weights":
+        weights = False
+    assert _create(g, L, weights) == ssc.E_INVALID_ARG
+
+
+def test_calls_reject_null_handle():
+    lib = ssc.lib()
+    p = E.Pillars(None, None, 0)
+    assert lib.sscater_step(None, ctypes.byref(p), None) == ssc.E_INVALID_ARG
+    assert lib.sscater_read(None, 0, None, 0, None) == ssc.E_INVALID_ARG
+    assert lib.sscater_reset(None, None) == ssc.E_INVALID_ARG
+    assert lib.sscater_destroy(None) == ssc.E_INVALID_ARG
+    n = ctypes.c_int32()
+    assert lib.sscater_changed(None, 0, None, 0, ctypes.byref(n), None) == ssc.E_INVALID_ARG
+    st = E.Stats()
+    assert lib.sscater_stats(None, ctypes.byref(st), None) == ssc.E_INVALID_ARG
+
+
+def test_weight_marshalling_for_bf16():
+    w = np.array([1.0, -2.5, 0.15625], np.float32)
+    b = E.weights_to_dtype_bytes(w, "bf16")
+    assert b.dtype == np.uint16 and b.tolist() == [0x3F80, 0xC020, 0x3E20]
+    with pytest.raises(ValueError):
+        E.weights_to_dtype_bytes(np.array([0.1], np.float32), "bf16")

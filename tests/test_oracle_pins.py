@@ -317,3 +317,18 @@ def test_full_pass_lists_are_nonzero_cells():
     x = _toy_stream(9, 9, 3, 0, 12)[0]
     lists = oracle.changed_lists(np.zeros_like(x.view(np.uint32)), x.view(np.uint32), [1])
     np.testing.assert_array_equal(lists[0], np.flatnonzero(np.any(x != 0, axis=-1)))
+
+
+@pytest.mark.parametrize("s", [1, 2])
+def test_pair_counts_equal_sum_of_single_cell_footprints(s):
+    """Pairs counted in the gather direction equal the sum over changed cells of
+    their individual footprints (each pinned above by the dependency test)."""
+    rng = np.random.default_rng(30 + s)
+    for H, W in [(7, 9), (8, 8), (5, 12)]:
+        mask = rng.random((H, W)) < 0.3
+        expect = 0
+        for p in np.flatnonzero(mask):
+            single = np.zeros((H, W), dtype=bool)
+            single.flat[p] = True
+            expect += int(oracle.propagate_gather(single, s).sum())
+        assert oracle.pair_counts(mask, s) == expect
