@@ -109,6 +109,7 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=20.0, help="time budget of the CPU oracle sample")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
+    ap.add_argument("--no-full", action="store_true", help="skip the GPU full-recompute timing")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -217,7 +218,7 @@ def main() -> int:
     # ---- GPU full recompute: reset + full window through the same kernels ----
     full = []
     last = dev[W + K]
-    for _ in range(5):
+    for _ in range(0 if args.no_full else 5):
         eng.reset()
         torch.cuda.synchronize()
         a = torch.cuda.Event(enable_timing=True)
@@ -227,7 +228,7 @@ def main() -> int:
         b.record(stream)
         torch.cuda.synchronize()
         full.append(a.elapsed_time(b))
-    full_ms = statistics.median(full)
+    full_ms = statistics.median(full) if full else None
     eng.close()
 
     cpu = None
@@ -254,7 +255,7 @@ def main() -> int:
         "alg_tflops": sum(2.0 * l.cin * l.cout * pairs[i + 1] for i, l in enumerate(wl.layers)) /
                       (wall_ms / 1e3) / 1e12,
         "full_recompute_ms": full_ms,
-        "speedup_vs_full_recompute": full_ms / ms_per_step,
+        "speedup_vs_full_recompute": full_ms / ms_per_step if full_ms else None,
         "kernels": {n: {"launches": k["launches"], "avg_us": k["ms"] / k["launches"] * 1e3}
                     for n, k in kernels.items()},
         "roofline": roofline,

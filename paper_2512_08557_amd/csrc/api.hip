@@ -229,7 +229,7 @@ int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_
     h->row_bytes = row_bytes;
     if (const char* g = getenv("SSCATER_LAYER_GRID")) {
         const int v = atoi(g);
-        if (v >= 8 && v <= 65536) h->layer_grid = v & ~7;
+        if (v >= 32 && v <= 65536) h->layer_grid = v & ~31;
     }
     hipError_t he = hipGetDevice(&h->device);
     if (he != hipSuccess) {
@@ -356,6 +356,7 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
         LayerArgs a{};
         a.list = ls.list;
         a.count = cnt + l;
+        a.cap = ls.Hout * ls.Wout;
         a.map_in = l == 1 ? h->map0 : h->layers[l - 2].map;
         a.delta_in = l == 1 ? h->delta0 : h->layers[l - 2].delta;
         a.wpack = ls.wpack;

@@ -45,26 +45,32 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
             }
         }
         // presence stamps: a pillar marks its cell present for this stride;
-        // a second pillar on the same cell is an input fault.
-        uint32_t st = 0;
+        // a second pillar on the same cell is an input fault.  The canvas and
+        // feature rows are fetched in the same round trip as the stamp.
+        // Loads are unconditional from clamped addresses (selected afterwards):
+        // a load inside a divergent branch makes the compiler drain all
+        // outstanding loads where the branch ends.
+        const int pc = act ? p : 0;
+        uint32_t st;   // read only from the group leader, which set it whenever act holds
         if (act && sub == 0) st = VANISH ? a.pres[p] : atomicExch(&a.pres[p], a.epoch);
+        char* xrow = static_cast<char*>(a.X) + (size_t)pc * ROWB + sub * 16;
+        uint4 ov = *reinterpret_cast<const uint4*>(xrow);
+        uint4 nv = make_uint4(0u, 0u, 0u, 0u);
+        if (!VANISH)
+            nv = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.feats) +
+                                                 (size_t)min(i, a.count - 1) * ROWB + sub * 16);
         st = __shfl(st, gbase);
         if (act && st == a.epoch) {
             if (!VANISH && sub == 0) flag_error(a.err, ERR_DUPLICATE);
             act = false;
         }
-        uint4 nv = make_uint4(0u, 0u, 0u, 0u), ov = make_uint4(0u, 0u, 0u, 0u);
-        char* xrow = static_cast<char*>(a.X) + (size_t)(act ? p : 0) * ROWB + sub * 16;
-        if (act) {
-            ov = *reinterpret_cast<const uint4*>(xrow);
-            if (!VANISH)
-                nv = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.feats) + (size_t)i * ROWB +
-                                                     sub * 16);
-        }
         const bool d = act && (nv.x != ov.x || nv.y != ov.y || nv.z != ov.z || nv.w != ov.w);
         const unsigned long long bal = __ballot(d);
         const unsigned long long gm = (G == 64 ? ~0ull : ((1ull << G) - 1ull)) << gbase;
         const bool gd = (bal & gm) != 0ull;
+        // stamp the first layer's footprint while the A_0 slot is reserved
+        PropBatch<G> pb;
+        prop_issue<G, false>(a.next, pc, gd, sub, a.epoch, pb);
         int row = wave_append(a.count0, gd && sub == 0);
         row = __shfl(row, gbase);
         if (gd) {
@@ -87,7 +93,7 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
             }
         }
         if (!VANISH && a.prev_out && sub == 0 && i < a.count) a.prev_out[i] = act ? p : -1;
-        propagate_cells<G>(a.next, gd ? p : -1, sub, a.epoch);
+        prop_finish<G>(a.next, a.epoch, pb);
     }
 }
 

@@ -75,6 +75,87 @@ __device__ __forceinline__ void propagate_cells(const PropTarget& t, int cell, i
     if (lane_id() == 0 && npairs) atomicAdd(t.pairs, npairs);
 }
 
+// Two-phase form of propagate_cells for latency hiding: prop_issue computes
+// the footprint slots and issues the stamping atomics; prop_finish (later,
+// after unrelated work) counts the pairs, reserves all list slots of the
+// wavefront with a single atomic and writes the list and index-map entries.
+// Both must be reached by every lane of the wavefront.
+template <int G>
+struct PropBatch {
+    static constexpr int ITERS = (9 + G - 1) / G;
+    int q[ITERS];
+    uint32_t old[ITERS];   // stamp before this lane's atomic (owner iff < epoch)
+};
+
+// cell: a valid cell of the source grid (used for addressing even when
+// inactive); active: whether the cell really changed.
+// UNCOND = true: every lane issues its atomic unconditionally so that no
+// branch joins on the returned value (a join would make the compiler wait for
+// it right there).  A slot without a target stamps a clamped cell next to
+// `cell` with 0, which never changes a stamp (stamps only grow and epochs
+// start at 1); the addresses stay spread over the grid.  Use it where most
+// lanes are active.  UNCOND = false: inactive lanes issue nothing.
+template <int G, bool UNCOND>
+__device__ __forceinline__ void prop_issue(const PropTarget& t, int cell, bool active, int sub, uint32_t epoch,
+                                           PropBatch<G>& pb) {
+    const int i = cell / t.Win, j = cell - (cell / t.Win) * t.Win;
+#pragma unroll
+    for (int it = 0; it < PropBatch<G>::ITERS; ++it) {
+        const int k = sub + it * G;
+        const int m = k / 3, n = k - 3 * (k / 3);
+        int rn = i - m + 1, cn = j - n + 1;
+        bool ok = active && k < 9;
+        if (t.stride == 2) {
+            ok = ok && ((rn | cn) & 1) == 0;
+            rn >>= 1;
+            cn >>= 1;
+        }
+        ok = ok && rn >= 0 && rn < t.Hout && cn >= 0 && cn < t.Wout;
+        const int q = min(max(rn, 0), t.Hout - 1) * t.Wout + min(max(cn, 0), t.Wout - 1);
+        pb.q[it] = ok ? q : -1;
+        if (UNCOND) {
+            pb.old[it] = atomicMax(&t.stamp[q], ok ? epoch : 0u);
+        } else if (ok) {
+            // pb.old is read only where q >= 0; leaving it unset on the other
+            // path avoids a register copy that would wait for the atomic
+            pb.old[it] = atomicMax(&t.stamp[q], epoch);
+        }
+    }
+}
+
+template <int G>
+__device__ __forceinline__ void prop_finish(const PropTarget& t, uint32_t epoch, PropBatch<G>& pb) {
+    constexpr int IT = PropBatch<G>::ITERS;
+    const int lane = lane_id();
+    const unsigned long long lt = (1ull << lane) - 1ull;
+    unsigned long long ob[IT];
+    bool own[IT];
+    int pairs = 0, tot = 0;
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        own[it] = pb.q[it] >= 0 && pb.old[it] < epoch;
+        pairs += (int)__popcll(__ballot(pb.q[it] >= 0));
+        ob[it] = __ballot(own[it]);
+        tot += (int)__popcll(ob[it]);
+    }
+    int base = 0;
+    if (lane == 0) {
+        if (tot) base = atomicAdd(t.count, tot);
+        if (pairs) atomicAdd(t.pairs, pairs);
+    }
+    if (tot == 0) return;
+    base = __shfl(base, 0);
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        if (own[it]) {
+            const int r = base + (int)__popcll(ob[it] & lt);
+            t.list[r] = pb.q[it];
+            t.map[pb.q[it]] = ((uint64_t)epoch << 32) | (uint32_t)r;
+        }
+        base += (int)__popcll(ob[it]);
+    }
+}
+
 // fp32 -> bf16 bits, round to nearest even (finite values).
 __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
     uint32_t u = __float_as_uint(f);

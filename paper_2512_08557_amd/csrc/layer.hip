@@ -62,79 +62,139 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
 
     const int lane = (int)(threadIdx.x & 63u), wave = (int)(threadIdx.x >> 6);
     const int cl = lane & 15, g = lane >> 4;
-    const int n = *a.count;
+    const int G = (int)gridDim.x;                // a multiple of 32
 
-    if (a.cum_dst && blockIdx.x == 0)
+    // First tile without waiting for the count: runs of 4 consecutive tiles
+    // share an XCD (workgroup b runs on XCD b % 8); a bijection on [0, G).
+    const int b = (int)blockIdx.x;
+    int tile = ((b >> 5) << 5) + ((b & 7) << 2) + ((b >> 3) & 3);
+    const int n = *a.count;
+    int e = tile * 16 + cl;
+    // loads are unconditional, from clamped (always valid) addresses, with the
+    // result selected afterwards: a load inside a divergent branch makes the
+    // compiler drain every outstanding load at the branch's end
+    int qspec = a.list[min(e, a.cap - 1)];
+
+    if (a.cum_dst && b == 0)
         for (int i = (int)threadIdx.x; i < a.n_cum; i += (int)blockDim.x) a.cum_dst[i] += a.cum_src[i];
 
-    const int ntiles = (n + 15) >> 4;
-    const int xcd = (int)(blockIdx.x & 7u), slot = (int)(blockIdx.x >> 3);
-    const int wgs_per_xcd = (int)(gridDim.x >> 3);
-    const int tiles_per_xcd = (ntiles + 7) >> 3;
-    for (int k = slot; k < tiles_per_xcd; k += wgs_per_xcd) {
-        const int tile = xcd * tiles_per_xcd + k;
-        if (tile >= ntiles) break;
-        const int e = tile * 16 + cl;
+    const bool do_prop = a.has_next && wave == 0;
+    while (tile * 16 < n) {
         const bool vrow = e < n;
-        const int q = vrow ? a.list[e] : 0;
+        const int q = vrow ? qspec : 0;
         const int qr = q / a.Wout, qc = q - (q / a.Wout) * a.Wout;
 
+        // index-map lookups of the 9 input taps, all in flight together
+        uint64_t ev[9];
+        bool inb[9];
+#pragma unroll
+        for (int t = 0; t < 9; ++t) {
+            const int ir = S * qr + t / 3 - 1, ic = S * qc + t % 3 - 1;
+            inb[t] = vrow && ir >= 0 && ir < a.Hin && ic >= 0 && ic < a.Win;
+            const int irc = min(max(ir, 0), a.Hin - 1), icc = min(max(ic, 0), a.Win - 1);
+            ev[t] = a.map_in[irc * a.Win + icc];
+        }
+        float* zrow = a.Z + (size_t)q * COUT;
+        f4v zo[NCB];
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) zo[cb] = *reinterpret_cast<const f4v*>(zrow + (wave * NCB + cb) * 16 + 4 * g);
+        // next layer's change list: stamp the footprint in the same round trip
+        // as the index-map and map loads, append the new cells at the end
+        PropBatch<4> pb;
+        if (do_prop) prop_issue<4, true>(a.next, q, vrow, g, a.epoch, pb);
+        int rows[9];
+        bool any[9];
+#pragma unroll
+        for (int t = 0; t < 9; ++t) {
+            rows[t] = (inb[t] && (uint32_t)(ev[t] >> 32) == a.epoch) ? (int)(uint32_t)ev[t] : -1;
+            any[t] = __ballot(rows[t] >= 0) != 0ull;    // no changed input under this tap: skip it
+        }
+
+        const char* dbase = static_cast<const char*>(a.delta_in) + g * 16;
+        const uint4* wbase = static_cast<const uint4*>(a.wpack) + (size_t)wave * NCB * 64 + lane;
         f4v acc[NCB];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) acc[cb] = f4v{0.f, 0.f, 0.f, 0.f};
 
-        for (int t = 0; t < 9; ++t) {
-            const int m = t / 3, nn = t - 3 * (t / 3);
-            const int ir = S * qr + m - 1, ic = S * qc + nn - 1;
-            int row = -1;
-            if (vrow && ir >= 0 && ir < a.Hin && ic >= 0 && ic < a.Win) {
-                const uint64_t ev = a.map_in[ir * a.Win + ic];
-                if ((uint32_t)(ev >> 32) == a.epoch) row = (int)(uint32_t)ev;
-            }
-            if (__ballot(row >= 0) == 0ull) continue;   // no changed input under this tap
-            const char* arow = static_cast<const char*>(a.delta_in) + (size_t)(row < 0 ? 0 : row) * ROWB_IN + g * 16;
-            const uint4* wp = static_cast<const uint4*>(a.wpack) +
-                              ((size_t)t * NCH * NCBT + (size_t)wave * NCB) * 64 + lane;
-#pragma unroll 2
-            for (int c = 0; c < NCH; ++c) {
-                uint4 av = make_uint4(0u, 0u, 0u, 0u);
-                if (row >= 0) av = *reinterpret_cast<const uint4*>(arow + c * 64);
+        auto mfma_chunk = [&](const uint4 av, const uint4 (&bv)[NCB]) {
 #pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) {
-                    const uint4 bv = wp[((size_t)c * NCBT + cb) * 64];
-                    if constexpr (BF16) {
-                        bf8v A, B;
-                        __builtin_memcpy(&A, &bv, 16);
-                        __builtin_memcpy(&B, &av, 16);
-                        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B, acc[cb], 0, 0, 0);
-                    } else {
-                        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bv.x), __uint_as_float(av.x),
-                                                                     acc[cb], 0, 0, 0);
-                        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bv.y), __uint_as_float(av.y),
-                                                                     acc[cb], 0, 0, 0);
-                        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bv.z), __uint_as_float(av.z),
-                                                                     acc[cb], 0, 0, 0);
-                        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bv.w), __uint_as_float(av.w),
-                                                                     acc[cb], 0, 0, 0);
-                    }
+            for (int cb = 0; cb < NCB; ++cb) {
+                if constexpr (BF16) {
+                    bf8v A, B;
+                    __builtin_memcpy(&A, &bv[cb], 16);
+                    __builtin_memcpy(&B, &av, 16);
+                    acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B, acc[cb], 0, 0, 0);
+                } else {
+                    acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bv[cb].x), __uint_as_float(av.x),
+                                                                 acc[cb], 0, 0, 0);
+                    acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bv[cb].y), __uint_as_float(av.y),
+                                                                 acc[cb], 0, 0, 0);
+                    acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bv[cb].z), __uint_as_float(av.z),
+                                                                 acc[cb], 0, 0, 0);
+                    acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bv[cb].w), __uint_as_float(av.w),
+                                                                 acc[cb], 0, 0, 0);
+                }
+            }
+        };
+        if constexpr (NCH <= 4) {
+            // narrow inputs: the 9 * NCH (tap, chunk) steps are fully unrolled
+            // and both operands are prefetched PF steps ahead, so the weight
+            // and delta loads of later taps overlap the current MFMAs
+            constexpr int NSTEP = 9 * NCH;
+            constexpr int PF = NCB == 1 ? 12 : (NCB == 2 ? 8 : 6);
+            uint4 abuf[NSTEP];
+            uint4 bbuf[NSTEP][NCB];
+            auto issue = [&](int st) {
+                const int t = st / NCH, c = st % NCH;
+                abuf[st] = *reinterpret_cast<const uint4*>(dbase + (size_t)max(rows[t], 0) * ROWB_IN + c * 64);
+                const uint4* wp = wbase + ((size_t)t * NCH + c) * NCBT * 64;
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) bbuf[st][cb] = wp[cb * 64];
+            };
+#pragma unroll
+            for (int st = 0; st < PF && st < NSTEP; ++st) issue(st);
+#pragma unroll
+            for (int st = 0; st < NSTEP; ++st) {
+                if (st + PF < NSTEP) issue(st + PF);
+                const int t = st / NCH;
+                uint4 av = abuf[st];
+                if (rows[t] < 0) av = make_uint4(0u, 0u, 0u, 0u);
+                if (any[t]) mfma_chunk(av, bbuf[st]);
+                // keep the scheduler from hoisting later loads past this step
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        } else {
+            // wide inputs: one tap at a time, chunks streamed; latency is hidden
+            // by the many resident wavefronts of these larger layers
+            for (int t = 0; t < 9; ++t) {
+                if (!any[t]) continue;
+                const char* arow = dbase + (size_t)max(rows[t], 0) * ROWB_IN;
+                const uint4* wp = wbase + (size_t)t * NCH * NCBT * 64;
+#pragma unroll 4
+                for (int c = 0; c < NCH; ++c) {
+                    uint4 av = *reinterpret_cast<const uint4*>(arow + c * 64);
+                    if (rows[t] < 0) av = make_uint4(0u, 0u, 0u, 0u);
+                    uint4 bv[NCB];
+#pragma unroll
+                    for (int cb = 0; cb < NCB; ++cb) bv[cb] = wp[((size_t)c * NCBT + cb) * 64];
+                    mfma_chunk(av, bv);
                 }
             }
         }
 
         if (vrow) {
-            float* zrow = a.Z + (size_t)q * COUT;
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
                 const int co0 = (wave * NCB + cb) * 16 + 4 * g;
-                const f4v zo = *reinterpret_cast<const f4v*>(zrow + co0);
+                const f4v o = zo[cb];
                 f4v zn;
-                zn.x = zo.x + acc[cb].x;
-                zn.y = zo.y + acc[cb].y;
-                zn.z = zo.z + acc[cb].z;
-                zn.w = zo.w + acc[cb].w;
+                zn.x = o.x + acc[cb].x;
+                zn.y = o.y + acc[cb].y;
+                zn.z = o.z + acc[cb].z;
+                zn.w = o.w + acc[cb].w;
                 *reinterpret_cast<f4v*>(zrow + co0) = zn;
                 if (a.delta_out) {
-                    f4v yo = zo, yn = zn;
+                    f4v yo = o, yn = zn;
                     if (a.relu) {
                         yo.x = fmaxf(yo.x, 0.f); yo.y = fmaxf(yo.y, 0.f); yo.z = fmaxf(yo.z, 0.f); yo.w = fmaxf(yo.w, 0.f);
                         yn.x = fmaxf(yn.x, 0.f); yn.y = fmaxf(yn.y, 0.f); yn.z = fmaxf(yn.z, 0.f); yn.w = fmaxf(yn.w, 0.f);
@@ -159,7 +219,12 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
                 }
             }
         }
-        if (a.has_next && wave == 0) propagate_cells<4>(a.next, vrow ? q : -1, g, a.epoch);
+        if (do_prop) prop_finish<4>(a.next, a.epoch, pb);
+
+        tile += G;
+        e = tile * 16 + cl;
+        if (tile * 16 >= n) break;
+        qspec = a.list[min(e, a.cap - 1)];
     }
 }
 
@@ -180,7 +245,7 @@ bool layer_supported(int cin, int cout, int stride, bool /*bf16*/) {
 }
 
 hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, int grid, hipStream_t s) {
-    grid = grid < 8 ? 8 : (grid & ~7);
+    grid = grid < 32 ? 32 : (grid & ~31);   // the first-tile mapping needs a multiple of 32
 #define SSC_LAUNCH(CI, CO, S)                                                                               \
     if (cin == CI && cout == CO && stride == S) {                                                           \
         dim3 blk(64 * LayerShape<CO>::NW);                                                                  \

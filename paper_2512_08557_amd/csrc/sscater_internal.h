@@ -48,6 +48,7 @@ struct DetectArgs {
 struct LayerArgs {
     const int32_t* list;      // A_l (cells of the output grid)
     const int32_t* count;     // |A_l|
+    int cap;                  // capacity of `list` (cells of the output grid)
     const uint64_t* map_in;   // index map of A_{l-1} on the input grid
     const void* delta_in;     // packed deltas of layer l-1 in A_{l-1} order
     const void* wpack;        // weights repacked for the MFMA operand layout
