@@ -25,6 +25,9 @@ Printed: one JSON line with
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import statistics
@@ -41,6 +44,7 @@ import streams as S  # noqa: E402
 
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}   # dense MFMA peaks of MI355X
 PEAK_HBM_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.txt")
 METRIC = "ms per stride and changed-cell conv updates/s; fraction of HBM/MFMA roofline"
 
 
@@ -100,6 +104,144 @@ def cpu_baseline(wl, ws, strides, first, budget_s):
                       f"{t_total / n * 1e3:.1f} ms per stride)"}
 
 
+# --------------------------------------------------------------------------
+# rocprofv3 digests: per-kernel durations from a --kernel-trace csv, and the
+# HBM traffic of the dominant kernel from --pmc FETCH_SIZE / WRITE_SIZE runs
+# scaled by what the same counters read for a plain copy of known size.
+# --------------------------------------------------------------------------
+def kernel_source_digest() -> str:
+    """sha256 over the library's kernel sources: a measured traffic figure is
+    only reported while the kernels are the ones it was measured on."""
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2512_08557_amd", "csrc", "*"))):
+        if f.endswith((".hip", ".h")):
+            h.update(os.path.basename(f).encode())
+            with open(f, "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
+
+
+def read_traffic(kernel: str, workload: str):
+    """Measured HBM bytes per launch of `kernel`, or None when absent or stale."""
+    try:
+        kv = {}
+        with open(TRAFFIC_FILE) as fh:
+            for line in fh:
+                line = line.strip()
+                if line and not line.startswith("#"):
+                    k, _, v = line.partition(" ")
+                    kv[k] = v.strip()
+        if (kv.get("source_sha256") == kernel_source_digest() and kv.get("kernel") == kernel
+                and kv.get("workload") == workload):
+            return float(kv["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        pass
+    return None
+
+
+def short_kernel(name: str) -> str:
+    """'void ssc::layer_kernel<64, 64, 1, false>(ssc::LayerArgs)' -> 'layer_kernel<64,64,1,f32>'."""
+    base = name.split("(")[0].replace("void ", "").replace("ssc::", "")
+    if "<" not in base:
+        return base
+    fn, _, targs = base.partition("<")
+    t = [x.strip() for x in targs.rstrip(">").split(",")]
+    dt = lambda v: "bf16" if v == "true" else "f32"
+    if fn == "detect_kernel" and len(t) == 3:
+        return f"detect_kernel<{t[0]},{dt(t[1])},{'vanished' if t[2] == 'true' else 'present'}>"
+    if fn == "layer_kernel" and len(t) == 4:
+        return f"layer_kernel<{t[0]},{t[1]},{t[2]},{dt(t[3])}>"
+    return fn + "<" + ",".join(t) + ">"
+
+
+def launches_per_stride(kernel: str, wl) -> int:
+    if kernel.startswith("detect_kernel"):
+        return 1
+    return sum(1 for l in wl.layers if f"layer_kernel<{l.cin},{l.cout},{l.stride},{wl.dtype}>" == kernel)
+
+
+def _csv_rows(path):
+    with open(path, newline="") as fh:
+        return list(csv.DictReader(fh))
+
+
+def digest_trace(path: str, steps: int, warmup: int, wl) -> str:
+    """Markdown tables of a --kernel-trace csv of the default bench command
+    (full window, warmup, timed strides, then the same strides again with HIP
+    events around every launch, then the full recomputes)."""
+    rows = sorted(_csv_rows(path), key=lambda r: int(r["Start_Timestamp"]))
+    by = {}
+    for r in rows:
+        by.setdefault(short_kernel(r["Kernel_Name"]), []).append(
+            (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    total = sum(sum(v) for v in by.values())
+    out = ["| Kernel | Calls | Avg (us) | Median (us) | Min (us) | Max (us) | Share |",
+           "|---|---|---|---|---|---|---|"]
+    for k, v in sorted(by.items(), key=lambda kv: -sum(kv[1])):
+        out.append(f"| {k} | {len(v)} | {statistics.fmean(v):.2f} | {statistics.median(v):.2f} | {min(v):.2f} | "
+                   f"{max(v):.2f} | {100 * sum(v) / total:.2f} % |")
+    out += ["", "| Kernel | Timed strides: avg (us) | Event-timed pass: avg (us) |", "|---|---|---|"]
+    for k, v in sorted(by.items()):
+        n = launches_per_stride(k, wl)
+        if n == 0:
+            continue
+        first = 0 if k.endswith("vanished>") else 1   # no vanish pass on a full window
+        a0, a1 = (first + warmup) * n, (first + warmup + steps) * n
+        b0, b1 = (2 * first + 2 * warmup + steps) * n, (2 * first + 2 * warmup + 2 * steps) * n
+        if len(v) >= b1:
+            out.append(f"| {k} | {statistics.fmean(v[a0:a1]):.2f} | {statistics.fmean(v[b0:b1]):.2f} |")
+    return "\n".join(out)
+
+
+def digest_pmc(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_bytes, kernel, per_stride,
+               steps, workload) -> str:
+    """HBM bytes per launch of `kernel` over the timed strides (the last
+    steps*per_stride dispatches), FETCH_SIZE and WRITE_SIZE each scaled by the
+    ratio of the copy's true size to what the counter reads for it."""
+    def per_kernel(path, name_pred):
+        vals = [float(r["Counter_Value"]) for r in sorted(_csv_rows(path), key=lambda r: int(r["Dispatch_Id"]))
+                if name_pred(r["Kernel_Name"])]
+        return vals
+    fk = per_kernel(fetch_csv, lambda n: short_kernel(n) == kernel)[-steps * per_stride:]
+    wk = per_kernel(write_csv, lambda n: short_kernel(n) == kernel)[-steps * per_stride:]
+    cf = per_kernel(copy_fetch_csv, lambda n: "copyBuffer" in n)
+    cw = per_kernel(copy_write_csv, lambda n: "copyBuffer" in n)
+    cf_kib, cw_kib = max(cf), max(cw)
+    f_scale, w_scale = copy_bytes / (cf_kib * 1024.0), copy_bytes / (cw_kib * 1024.0)
+    fetch, write = statistics.fmean(fk), statistics.fmean(wk)
+    traffic = fetch * 1024.0 * f_scale + write * 1024.0 * w_scale
+    lines = [
+        "# HBM traffic per launch of the dominant kernel (rocprofv3 --pmc FETCH_SIZE, WRITE_SIZE)",
+        f"source_sha256 {kernel_source_digest()}",
+        f"kernel {kernel}",
+        f"workload {workload}",
+        f"dispatches {len(fk)}",
+        f"fetch_kib_per_launch {fetch:.3f}",
+        f"write_kib_per_launch {write:.3f}",
+        f"copy_bytes {copy_bytes}",
+        f"copy_fetch_kib {cf_kib:.3f}",
+        f"copy_write_kib {cw_kib:.3f}",
+        f"fetch_scale {f_scale:.5f}",
+        f"write_scale {w_scale:.5f}",
+        f"traffic_bytes_per_launch {traffic:.1f}",
+    ]
+    return "\n".join(lines) + "\n"
+
+
+def copy_calibration(nbytes: int) -> int:
+    """A plain device-to-device copy of nbytes (the counters' calibration)."""
+    import torch
+    torch.cuda.set_device(0)
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"[bench] copied {nbytes} bytes 3 times")
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -110,7 +252,26 @@ def main() -> int:
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
     ap.add_argument("--no-full", action="store_true", help="skip the GPU full-recompute timing")
+    ap.add_argument("--copy-bytes", type=int, default=0,
+                    help="only run a plain device copy of this many bytes (counter calibration)")
+    ap.add_argument("--digest-trace", metavar="CSV", help="summarise a rocprofv3 kernel-trace csv and exit")
+    ap.add_argument("--digest-pmc", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
+                    help="turn rocprofv3 --pmc csvs into the traffic record of the dominant kernel and exit")
+    ap.add_argument("--kernel", default="layer_kernel<64,64,1,f32>", help="kernel of --digest-pmc")
     args = ap.parse_args()
+
+    if args.digest_trace:
+        print(digest_trace(args.digest_trace, args.steps, args.warmup, S.workload(args.workload)))
+        return 0
+    if args.digest_pmc:
+        per = launches_per_stride(args.kernel, S.workload(args.workload))
+        rec = digest_pmc(*args.digest_pmc, args.copy_bytes, args.kernel, max(per, 1), args.steps, args.workload)
+        with open(TRAFFIC_FILE, "w") as fh:
+            fh.write(rec)
+        print(rec)
+        return 0
+    if args.copy_bytes:
+        return copy_calibration(args.copy_bytes)
 
     if args.gpus != 1:
         log("bench.py: this build runs on one GPU only; multi-GPU runs are not supported "

@@ -22,7 +22,7 @@
  *     input delta at a marked site is phi(Z_new) - phi(Z_old).
  *
  * The result after every stride equals recomputing each layer's convolution
- * from scratch on the whole window (abstract; Sec. V-A), up to floating-point
+ * from scratch on the whole window (abstract; Sec. IV-G), up to floating-point
  * summation order.
  *
  * Conventions

@@ -8,7 +8,7 @@ What it computes (SSCATeR, arXiv 2512.08557):
 
 * ``forward``: every backbone layer recomputed densely from the window's input
   canvas in float64 (``sscater_oracle.c``).  The paper states that the recycled
-  maps are identical to recomputation (abstract; Sec. V-A), so recomputation is
+  maps are identical to recomputation (abstract; Sec. IV-G), so recomputation is
   the reference for the maps.
 * ``changed_lists``: the per-layer changed-cell sets.  The input set A_0 is the
   set of cells whose input feature vector differs bit for bit from the previous

@@ -7,7 +7,7 @@
  *
  * SSCATeR (arXiv 2512.08557) claims that its recycled convolution maps are
  * identical to recomputing the sparse / dense convolution from scratch
- * (abstract; Sec. V-A "Performance and Results Evaluation"; Sec. V-B).  So the
+ * (abstract; Sec. IV-G "Performance and Results Evaluation"; Sec. V).  So the
  * oracle does not model the method at all: for one window it recomputes every
  * backbone layer densely, in double precision, from the input canvas.
  *

@@ -11,7 +11,7 @@ Paper context (SSCATeR, arXiv 2512.08557):
   * pillar grid of 0.16 m cells, pseudo-image of C=64 channels, up to P=12,000
     pillars (Sec. III-B);
   * 100 ms window advanced in 10 ms strides, each stride corresponding to a
-    36 degree wedge of a rotating sensor (Sec. I / II);
+    36 degree wedge of a rotating sensor (Sec. I; Sec. II-C);
   * backbone of three Block(S, L, F) with S=2, L=4/6/6, F=64/128/256
     (Sec. III-B, backbone paragraph).
 The real drone datasets are not available; these seeded scenes stand in for

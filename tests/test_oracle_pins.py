@@ -238,7 +238,7 @@ def _toy_stream(H, W, C0, n, seed, toggles=True, refresh=0.05):
     [(4, 5, 1, True), (5, 5, 2, True), (5, 4, 2, False)],
 ])
 def test_method_model_equals_recompute(layers):
-    """The recycling claim (abstract; Sec. V-A): after many delta strides with
+    """The recycling claim (abstract; Sec. IV-G): after many delta strides with
     refreshes and toggles, the recycled maps equal recomputation."""
     H, W, C0 = 13, 11, 4
     rng = np.random.default_rng(99)
