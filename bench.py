@@ -166,9 +166,10 @@ def _csv_rows(path):
 
 
 def digest_trace(path: str, steps: int, warmup: int, wl) -> str:
-    """Markdown tables of a --kernel-trace csv of the default bench command
-    (full window, warmup, timed strides, then the same strides again with HIP
-    events around every launch, then the full recomputes)."""
+    """Markdown tables of a --kernel-trace csv of the default bench command:
+    three passes of (full window, warmup, the timed strides) -- timed, with an
+    event after every stride, with events around every launch -- then the
+    full recomputes."""
     rows = sorted(_csv_rows(path), key=lambda r: int(r["Start_Timestamp"]))
     by = {}
     for r in rows:
@@ -186,8 +187,9 @@ def digest_trace(path: str, steps: int, warmup: int, wl) -> str:
         if n == 0:
             continue
         first = 0 if k.endswith("vanished>") else 1   # no vanish pass on a full window
+        span = (first + warmup + steps) * n            # launches of one pass
         a0, a1 = (first + warmup) * n, (first + warmup + steps) * n
-        b0, b1 = (2 * first + 2 * warmup + steps) * n, (2 * first + 2 * warmup + 2 * steps) * n
+        b0, b1 = 2 * span + a0, 2 * span + a1          # third pass: events around every launch
         if len(v) >= b1:
             out.append(f"| {k} | {statistics.fmean(v[a0:a1]):.2f} | {statistics.fmean(v[b0:b1]):.2f} |")
     return "\n".join(out)
@@ -303,19 +305,26 @@ def main() -> int:
     torch.cuda.synchronize()
     before = eng.stats()
 
-    # ---- timed region: exactly K delta strides ----
+    # ---- timed region: exactly K delta strides, nothing else on the stream ----
     stream = torch.cuda.current_stream()
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    run_range(1 + W, 1 + W + K)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    after = eng.stats()
+    wall_ms = (t1 - t0) * 1e3
+
+    # ---- latency pass: the same strides again, a HIP event after each ----
+    eng.reset()
+    run_range(0, 1 + W)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    torch.cuda.synchronize()
     evs[0].record(stream)
     for k in range(K):
         eng.step(*dev[1 + W + k])
         evs[k + 1].record(stream)
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    after = eng.stats()
-    wall_ms = (t1 - t0) * 1e3
     per_stride = [evs[k].elapsed_time(evs[k + 1]) for k in range(K)]
     act_in = [after["active_total"][l] - before["active_total"][l] for l in range(L + 1)]
     pairs = [after["pairs_total"][l] - before["pairs_total"][l] for l in range(L + 1)]
@@ -410,6 +419,7 @@ def main() -> int:
                    "strides": "full window + warmup untimed, then the timed delta strides",
                    "mean_pillars": float(np.mean([len(s.idx) for s in strides[1 + W:]])),
                    "mean_active": [a / K for a in act_in]},
+        # per-stride latency from a second pass with an event after every stride
         "latency_ms": {"mean": statistics.fmean(per_stride), "p50": srt[len(srt) // 2],
                        "p99": srt[min(len(srt) - 1, int(0.99 * len(srt)))], "max": srt[-1],
                        "over_10ms_frac": sum(1 for x in per_stride if x > 10.0) / K},

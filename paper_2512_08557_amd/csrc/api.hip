@@ -10,11 +10,12 @@
 // Work sizes live in device counters; the layer kernels walk their tiles from
 // the counter, so the host never waits for a count.
 //
-// Every change list is a set of cells stamped with the stride's epoch in a
-// per-grid stamp map; a map entry (epoch << 32 | row) locates the cell's row in
-// the packed delta buffer.  Bumping the epoch invalidates every list at once,
-// so no per-stride clears are needed.  The two counter sets alternate between
-// strides; the detect launch clears the set the next stride will use.
+// Every change set is the set of cells stamped with the stride's epoch in a
+// per-grid stamp map, and every delta row sits at its cell's position;
+// bumping the epoch invalidates every set at once, so no per-stride clears are
+// needed.  The output sets of the layers are also compacted into lists of
+// NSHARD segments.  The two counter sets alternate between strides; the
+// detect launch clears the set the next stride will use.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -37,9 +38,8 @@ struct LayerState {
     float* Z = nullptr;
     void* wpack = nullptr;
     uint32_t* stamp = nullptr;
-    uint64_t* map = nullptr;
-    int32_t* list = nullptr;
-    void* delta = nullptr;   // packed deltas of this layer's output (nullptr for the last layer)
+    int32_t* list = nullptr; // NSHARD segments of Hout*Wout cells
+    void* delta = nullptr;   // deltas of this layer's output, dense by cell (nullptr for the last layer)
 };
 
 thread_local char g_hip_err[256] = "no HIP error";
@@ -63,20 +63,20 @@ struct sscater {
     int row_bytes = 0;      // bytes of one input feature row
     LayerState layers[SSCATER_MAX_LAYERS];
     void* X = nullptr;
-    uint32_t* pres = nullptr;
-    uint64_t* map0 = nullptr;
-    int32_t* list0 = nullptr;
+    uint64_t* pres = nullptr;
+    uint32_t* stamp0 = nullptr;
     void* delta0 = nullptr;
     int32_t* prev[2] = {nullptr, nullptr};
     int prev_slot = 0;
     int32_t prev_count = 0;
     bool prev_dense = false;
-    int32_t* counters = nullptr;   // [2][2*(L+1)]: per set cnt[0..L], pairs[0..L]
-    long long* cum = nullptr;      // [2*(L+1)]
+    int32_t* counters = nullptr;   // [2][2*(L+1)][NSHARD][CSTRIDE]: per set cnt[0..L][shard], pairs[0..L][shard]
+    long long* cum = nullptr;      // running totals, same layout as one set
     int32_t* err_host = nullptr;   // host-visible sticky error word
     int32_t* err_dev = nullptr;
     uint32_t epoch = 0;
     int last_set = -1;             // counter set of the last stride, -1 after create/reset
+    uint32_t last_epoch = 0;       // epoch of the last stride
     long long steps = 0;
     int32_t last_pillars = 0;
     int layer_grid = 1024;
@@ -91,7 +91,9 @@ struct sscater {
     size_t ev_next = 0;
     std::vector<ProfRec> prof_recs;
 
-    int ncnt() const { return 2 * (L + 1); }
+    int ncnt() const { return 2 * (L + 1) * NSHARD * CSTRIDE; }
+    int32_t* cnt_ptr(int set, int l) { return set_ptr(set) + (size_t)l * NSHARD * CSTRIDE; }
+    int32_t* pairs_ptr(int set, int l) { return set_ptr(set) + (size_t)(L + 1 + l) * NSHARD * CSTRIDE; }
     int32_t* set_ptr(int s) { return counters + (size_t)s * ncnt(); }
 };
 
@@ -171,10 +173,9 @@ PropTarget prop_target(sscater* h, int l /* consuming layer, 1..L */, int set) {
     t.Hout = ls.Hout;
     t.Wout = ls.Wout;
     t.stamp = ls.stamp;
-    t.map = ls.map;
     t.list = ls.list;
-    t.count = h->set_ptr(set) + l;
-    t.pairs = h->set_ptr(set) + (h->L + 1) + l;
+    t.count = h->cnt_ptr(set, l);
+    t.pairs = h->pairs_ptr(set, l);
     return t;
 }
 
@@ -246,10 +247,9 @@ int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_
         if (rc != SSCATER_OK) goto fail; \
     } while (0)
     SSC_TRY(dev_alloc(h, &h->X, cells * row_bytes));
-    SSC_TRY(dev_alloc(h, (void**)&h->pres, cells * 4));
-    SSC_TRY(dev_alloc(h, (void**)&h->map0, cells * 8));
-    SSC_TRY(dev_alloc(h, (void**)&h->list0, cells * 4));
-    // A_0 holds at most every cell (dense mode); fp32 rows or bf16 [new | old] pairs
+    SSC_TRY(dev_alloc(h, (void**)&h->pres, cells * 8));
+    SSC_TRY(dev_alloc(h, (void**)&h->stamp0, cells * 4));
+    // input deltas dense by cell: fp32 rows or bf16 [new | old] pairs
     SSC_TRY(dev_alloc(h, &h->delta0, cells * (size_t)(bf16 ? 2 * row_bytes : row_bytes)));
     SSC_TRY(dev_alloc(h, (void**)&h->prev[0], (size_t)grid->max_pillars * 4));
     SSC_TRY(dev_alloc(h, (void**)&h->prev[1], (size_t)grid->max_pillars * 4));
@@ -267,8 +267,7 @@ int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_
             const size_t oc = (size_t)ls.Hout * ls.Wout;
             SSC_TRY(dev_alloc(h, (void**)&ls.Z, oc * ls.spec.cout * 4));
             SSC_TRY(dev_alloc(h, (void**)&ls.stamp, oc * 4));
-            SSC_TRY(dev_alloc(h, (void**)&ls.map, oc * 8));
-            SSC_TRY(dev_alloc(h, (void**)&ls.list, oc * 4));
+            SSC_TRY(dev_alloc(h, (void**)&ls.list, oc * 4 * NSHARD));
             if (l + 1 < n_layers) SSC_TRY(dev_alloc(h, &ls.delta, oc * ls.spec.cout * 4));
             const size_t wn = wpack_elems(ls.spec.cin, ls.spec.cout, bf16);
             std::vector<unsigned char> packed(wn * esz);
@@ -327,9 +326,8 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
     d.prev_out = dense ? nullptr : h->prev[cur_slot];
     d.X = h->X;
     d.pres = h->pres;
-    d.map0 = h->map0;
-    d.list0 = h->list0;
-    d.count0 = cnt;
+    d.stamp0 = h->stamp0;
+    d.count0 = h->cnt_ptr(set, 0);
     d.delta0 = h->delta0;
     d.zero_ptr = h->set_ptr(set ^ 1);
     d.zero_n = h->ncnt();
@@ -340,10 +338,15 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
     hipError_t e = timed_launch(h, 0, s, [&] { return launch_detect_present(d, h->row_bytes, h->bf16, s); });
     if (e != hipSuccess) return hip_fail(e);
 
-    if (!dense && (h->prev_dense || h->prev_count > 0)) {
+    // vanished cells of the previous list, and the ownership check of the
+    // new list's presence words (pillar mode only: dense input has no
+    // duplicates)
+    if (!dense && (h->prev_dense || h->prev_count > 0 || pl->count > 0)) {
         DetectArgs v = d;
         v.prev = h->prev_dense ? nullptr : h->prev[h->prev_slot];
         v.count = h->prev_dense ? (int32_t)cells : h->prev_count;
+        v.chk_idx = pl->count > 0 ? pl->idx : nullptr;
+        v.chk_count = pl->count;
         v.prev_out = nullptr;
         v.zero_ptr = nullptr;
         v.zero_n = 0;
@@ -355,9 +358,9 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
         LayerState& ls = h->layers[l - 1];
         LayerArgs a{};
         a.list = ls.list;
-        a.count = cnt + l;
+        a.count = h->cnt_ptr(set, l);
         a.cap = ls.Hout * ls.Wout;
-        a.map_in = l == 1 ? h->map0 : h->layers[l - 2].map;
+        a.stamp_in = l == 1 ? h->stamp0 : h->layers[l - 2].stamp;
         a.delta_in = l == 1 ? h->delta0 : h->layers[l - 2].delta;
         a.wpack = ls.wpack;
         a.Z = ls.Z;
@@ -390,6 +393,7 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
         h->prev_dense = true;
     }
     h->last_set = set;
+    h->last_epoch = epoch;
     h->steps += 1;
     h->last_pillars = pl->count;
     return SSCATER_OK;
@@ -433,7 +437,7 @@ int sscater_reset(sscater_t h, void* stream) {
     if (e == hipSuccess) e = launch_fill_zero(h->counters, round_up((size_t)2 * h->ncnt() * 4, 256), s);
     if (e == hipSuccess) e = launch_fill_zero(h->cum, round_up((size_t)h->ncnt() * 8, 256), s);
     if (e != hipSuccess) return hip_fail(e);
-    ++h->epoch;   // every stamp and index map becomes stale
+    ++h->epoch;   // every stamp becomes stale
     h->prev_count = 0;
     h->prev_dense = false;
     h->last_set = -1;
@@ -466,15 +470,34 @@ int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32
         *count_host = 0;
         return SSCATER_OK;
     }
-    int32_t n = 0;
-    e = hipMemcpy(&n, h->set_ptr(h->last_set) + layer, 4, hipMemcpyDeviceToHost);
+    int32_t cnt[NSHARD * CSTRIDE];
+    e = hipMemcpy(cnt, h->cnt_ptr(h->last_set, layer), sizeof cnt, hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(e);
+    std::vector<int32_t> buf;
+    if (layer == 0) {
+        // A_0 is the set of input cells stamped with the last stride's epoch
+        const int cells = h->grid.H * h->grid.W;
+        std::vector<uint32_t> st((size_t)cells);
+        e = hipMemcpy(st.data(), h->stamp0, st.size() * 4, hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(e);
+        for (int q = 0; q < cells; ++q)
+            if (st[(size_t)q] == h->last_epoch) buf.push_back(q);
+    } else {
+        // the list segments; a segment never holds more entries than its grid has cells
+        const LayerState& ls = h->layers[layer - 1];
+        const int cap_cells = ls.Hout * ls.Wout;
+        for (int k = 0; k < NSHARD; ++k) {
+            const int m = std::min(std::max(cnt[k * CSTRIDE], 0), cap_cells);
+            if (m == 0) continue;
+            const size_t at = buf.size();
+            buf.resize(at + (size_t)m);
+            e = hipMemcpy(buf.data() + at, ls.list + (size_t)k * cap_cells, (size_t)m * 4, hipMemcpyDeviceToHost);
+            if (e != hipSuccess) return hip_fail(e);
+        }
+    }
+    const int32_t n = (int32_t)buf.size();
     *count_host = n;
     if (n == 0) return SSCATER_OK;
-    std::vector<int32_t> buf((size_t)n);
-    const int32_t* src = layer == 0 ? h->list0 : h->layers[layer - 1].list;
-    e = hipMemcpy(buf.data(), src, (size_t)n * 4, hipMemcpyDeviceToHost);
-    if (e != hipSuccess) return hip_fail(e);
     std::sort(buf.begin(), buf.end());
     std::memcpy(dst, buf.data(), (size_t)std::min(n, cap) * 4);
     return SSCATER_OK;
@@ -500,29 +523,39 @@ int sscater_stats(sscater_t h, sscater_stats_t* out, void* stream) {
     }
     e = hipMemcpy(t.data(), h->cum, t.size() * 8, hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(e);
+    std::vector<long long> act(L + 1, 0), prs(L + 1, 0);
     for (int l = 0; l <= L; ++l) {
-        out->active[l] = c[l];
-        out->pairs[l] = c[L + 1 + l];
-        out->active_total[l] = t[l];
-        out->pairs_total[l] = t[L + 1 + l];
+        long long a_c = 0, p_c = 0, a_t = 0, p_t = 0;
+        for (int k = 0; k < NSHARD; ++k) {
+            a_c += c[((size_t)l * NSHARD + k) * CSTRIDE];
+            p_c += c[((size_t)(L + 1 + l) * NSHARD + k) * CSTRIDE];
+            a_t += t[((size_t)l * NSHARD + k) * CSTRIDE];
+            p_t += t[((size_t)(L + 1 + l) * NSHARD + k) * CSTRIDE];
+        }
+        act[l] = a_c;
+        prs[l] = p_c;
+        out->active[l] = (int32_t)a_c;
+        out->pairs[l] = (int32_t)p_c;
+        out->active_total[l] = a_t;
+        out->pairs_total[l] = p_t;
     }
     // algorithmic flops and HBM bytes of the last stride (the method's own work)
     const double e_in = h->bf16 ? 2.0 : 4.0;        // stored feature element
-    const double e_d = 4.0;                          // packed delta element (fp32, or bf16 pair)
+    const double e_d = 4.0;                          // delta element (fp32, or bf16 pair)
     const double P = (double)h->last_pillars, C0 = (double)h->grid.C0;
     double flops = 0.0;
     double bytes = P * (4.0 + C0 * e_in)             // new pillar list
                    + P * C0 * e_in                   // canvas compare gather
-                   + (double)c[0] * C0 * (e_in + e_d);  // canvas write + packed input deltas
+                   + (double)act[0] * C0 * (e_in + e_d);  // canvas write + input deltas
     for (int l = 1; l <= L; ++l) {
         const sscater_layer& sp = h->layers[l - 1].spec;
-        const double a_in = c[l - 1], a_out = c[l], pairs = c[L + 1 + l];
+        const double a_in = (double)act[l - 1], a_out = (double)act[l], pairs = (double)prs[l];
         flops += 2.0 * sp.cin * sp.cout * pairs;
-        bytes += a_in * sp.cin * e_d                 // packed input deltas
+        bytes += a_in * sp.cin * e_d                 // input deltas
                  + a_out * sp.cout * 8.0             // Z read + write
                  + (l < L ? a_out * sp.cout * e_d : 0.0)   // emitted deltas
                  + 9.0 * sp.cin * sp.cout * e_in     // weights
-                 + 12.0 * (a_in + a_out);            // lists and index maps
+                 + 8.0 * (a_in + a_out);             // lists and stamps
     }
     out->flops = flops;
     out->bytes = bytes;

@@ -11,74 +11,16 @@ typedef __bf16 bf8v __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ int lane_id() { return (int)(threadIdx.x & 63u); }
 
-// Append one entry per lane whose `pred` is set to a device list whose length
-// is *counter: one atomic per wavefront, positions in lane order.  Must be
-// reached by every lane of the wavefront.  Returns the lane's slot or -1.
-__device__ __forceinline__ int wave_append(int32_t* counter, bool pred) {
-    const unsigned long long m = __ballot(pred);
-    if (m == 0ull) return -1;
-    const int lane = lane_id();
-    const int leader = __ffsll((long long)m) - 1;
-    int base = 0;
-    if (lane == leader) base = atomicAdd(counter, (int)__popcll(m));
-    base = __shfl(base, leader);
-    const int rank = (int)__popcll(m & ((1ull << lane) - 1ull));
-    return pred ? base + rank : -1;
-}
-
-__device__ __forceinline__ int wave_sum(int v) {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    return v;
-}
-
-// Structural propagation of changed cells to the next layer's list.
-// Cell `cell` of the grid (t.Hin x t.Win) (or -1 for none) feeds output
-// ((i - m + 1)/s, (j - n + 1)/s) through tap (m, n) when both quotients are
-// integral and inside (t.Hout x t.Wout): the scatter target of Eq. 2
+// Structural propagation of changed cells to the next layer's list, in two
+// phases for latency hiding.  Cell (i, j) of the grid (t.Hin x t.Win) feeds
+// output ((i - m + 1)/s, (j - n + 1)/s) through tap (m, n) when both quotients
+// are integral and inside (t.Hout x t.Wout): the scatter target of Eq. 2
 // generalised to stride s, and the downsampling rule of Alg. 1 for s = 2.
-// Each cell is handled by G lanes that share the 9 tap slots (slot = sub +
-// it*G).  Every touched output cell is stamped with `epoch`; the first lane
-// to stamp it appends it to t.list and records its position in t.map.  The
-// number of (cell, tap) pairs with an in-grid target is added to *t.pairs.
-// Must be reached by every lane of the wavefront.
-template <int G>
-__device__ __forceinline__ void propagate_cells(const PropTarget& t, int cell, int sub, uint32_t epoch) {
-    constexpr int ITERS = (9 + G - 1) / G;
-    int npairs = 0;
-#pragma unroll
-    for (int it = 0; it < ITERS; ++it) {
-        const int k = sub + it * G;
-        int q = -1;
-        if (cell >= 0 && k < 9) {
-            const int i = cell / t.Win, j = cell - (cell / t.Win) * t.Win;
-            const int m = k / 3, n = k - 3 * (k / 3);
-            int rn = i - m + 1, cn = j - n + 1;     // >= -1
-            bool ok = true;
-            if (t.stride == 2) {
-                ok = ((rn | cn) & 1) == 0;
-                rn >>= 1;
-                cn >>= 1;
-            }
-            if (ok && rn >= 0 && rn < t.Hout && cn >= 0 && cn < t.Wout) q = rn * t.Wout + cn;
-        }
-        npairs += (q >= 0) ? 1 : 0;
-        bool own = false;
-        if (q >= 0) own = atomicMax(&t.stamp[q], epoch) < epoch;
-        const int r = wave_append(t.count, own);
-        if (own) {
-            t.list[r] = q;
-            t.map[q] = ((uint64_t)epoch << 32) | (uint32_t)r;
-        }
-    }
-    npairs = wave_sum(npairs);
-    if (lane_id() == 0 && npairs) atomicAdd(t.pairs, npairs);
-}
-
-// Two-phase form of propagate_cells for latency hiding: prop_issue computes
-// the footprint slots and issues the stamping atomics; prop_finish (later,
-// after unrelated work) counts the pairs, reserves all list slots of the
-// wavefront with a single atomic and writes the list and index-map entries.
+// Each cell is handled by G lanes that share its 9 tap slots (slot = sub +
+// it*G).  prop_issue stamps every target with `epoch` (atomicMax: the lane
+// that moves a stamp owns the target); prop_finish (later, after unrelated
+// work) counts the pairs and appends the owned targets of the wavefront to
+// list segment `shard` with a single atomic.
 // Both must be reached by every lane of the wavefront.
 template <int G>
 struct PropBatch {
@@ -124,7 +66,7 @@ __device__ __forceinline__ void prop_issue(const PropTarget& t, int cell, bool a
 }
 
 template <int G>
-__device__ __forceinline__ void prop_finish(const PropTarget& t, uint32_t epoch, PropBatch<G>& pb) {
+__device__ __forceinline__ void prop_finish(const PropTarget& t, uint32_t epoch, int shard, PropBatch<G>& pb) {
     constexpr int IT = PropBatch<G>::ITERS;
     const int lane = lane_id();
     const unsigned long long lt = (1ull << lane) - 1ull;
@@ -140,18 +82,15 @@ __device__ __forceinline__ void prop_finish(const PropTarget& t, uint32_t epoch,
     }
     int base = 0;
     if (lane == 0) {
-        if (tot) base = atomicAdd(t.count, tot);
-        if (pairs) atomicAdd(t.pairs, pairs);
+        if (tot) base = atomicAdd(t.count + shard * CSTRIDE, tot);
+        if (pairs) atomicAdd(t.pairs + shard * CSTRIDE, pairs);
     }
     if (tot == 0) return;
     base = __shfl(base, 0);
+    int32_t* seg = t.list + (size_t)shard * (t.Hout * t.Wout);
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
-        if (own[it]) {
-            const int r = base + (int)__popcll(ob[it] & lt);
-            t.list[r] = pb.q[it];
-            t.map[pb.q[it]] = ((uint64_t)epoch << 32) | (uint32_t)r;
-        }
+        if (own[it]) seg[base + (int)__popcll(ob[it] & lt)] = pb.q[it];
         base += (int)__popcll(ob[it]);
     }
 }

@@ -9,18 +9,19 @@
 //   * the change list A_l of this layer's OUTPUT grid was built by the
 //     previous launch (scatter rule), so every output cell that receives a
 //     scatter contribution is known up front;
-//   * a workgroup owns 16 consecutive cells of A_l and all output channels.
-//     For each of the 9 taps it gathers, through the epoch-stamped index map
-//     of A_{l-1}, the packed delta rows of the input cells under that tap
-//     (rows of unchanged input cells are zero and a tap with no changed input
-//     in the whole tile is skipped) and contracts them with the tap's weights
-//     on the matrix cores: D[cout x 16 cells] += W_t^T[cout x cin] . dY^T.
+//   * a workgroup owns 16 consecutive cells of one segment of A_l and all
+//     output channels.  For each of the 9 taps it checks the change stamps
+//     of the input cells under that tap and gathers the delta rows of the
+//     changed ones (stored at their cells; unchanged inputs contribute zero
+//     and a tap with no changed input in the whole tile is skipped), then
+//     contracts them with the tap's weights on the matrix cores:
+//     D[cout x 16 cells] += W_t^T[cout x cin] . dY^T.
 //     Summing the 9 taps per output cell in a fixed order is exactly the sum
 //     the scatter of Eq. 2 adds into that cell, so the result is
 //     deterministic and each Z row is read and written once per stride;
-//   * epilogue in registers: Z_new = Z_old + D; store Z_new; emit the next
-//     layer's packed delta row (fp32 phi(Z_new) - phi(Z_old), or the bf16 pair
-//     [bf16(phi(Z_new)) | bf16(phi(Z_old))]);
+//   * epilogue in registers: Z_new = Z_old + D; store Z_new; write the next
+//     layer's delta row at the cell (fp32 phi(Z_new) - phi(Z_old), or the bf16
+//     pair [bf16(phi(Z_new)) | bf16(phi(Z_old))]);
 //   * wavefront 0 then propagates the tile's cells to the next layer's change
 //     list (the structural rule, including stride-2 downsampling).
 //
@@ -34,12 +35,14 @@
 // fully coalesced; D is four consecutive output channels of one cell, so the Z
 // update is a 16-byte load/store per lane.
 //
-// Tiles are walked XCD-aware: workgroup b runs on XCD b % 8, and each XCD
-// takes a contiguous range of tiles so neighbouring cells (which share input
-// rows) meet in the same L2.
+// Workgroup b walks the tiles of list segment (b / 8) % NSHARD; the
+// segments are filled by different workgroups of the previous launch so that
+// no single counter takes every append.
 #include "device_common.h"
 
 #include <string.h>
+
+#include <algorithm>
 
 namespace ssc {
 
@@ -57,23 +60,32 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
     constexpr int KTOT = BF16 ? 2 * CIN : CIN;   // contraction length per tap
     constexpr int KCH = BF16 ? 32 : 16;          // k per 64-byte chunk
     constexpr int NCH = KTOT / KCH;
-    constexpr int ROWB_IN = 4 * CIN;             // packed input row bytes (fp32, or bf16 pair)
+    constexpr int ROWB_IN = 4 * CIN;             // input delta row bytes (fp32, or bf16 pair)
     constexpr int ROWB_OUT = 4 * COUT;
 
     const int lane = (int)(threadIdx.x & 63u), wave = (int)(threadIdx.x >> 6);
     const int cl = lane & 15, g = lane >> 4;
-    const int G = (int)gridDim.x;                // a multiple of 32
+    const int G = (int)gridDim.x;                // a multiple of 32 * NSHARD
 
-    // First tile without waiting for the count: runs of 4 consecutive tiles
-    // share an XCD (workgroup b runs on XCD b % 8); a bijection on [0, G).
+    // tiles of segment (b / 8) % NSHARD, first one without waiting for the
+    // count.  The workgroups of a segment sit on all eight XCDs (workgroup b
+    // runs on XCD b % 8), so an uneven split of the list over the segments
+    // does not load one XCD more than another, and runs of 4 consecutive
+    // tiles (neighbouring cells, which share input rows) share an XCD's L2:
+    // with x = b % 8 and h = b / (8 * NSHARD), the first tile is
+    // 32 * (h / 4) + 4 * x + h % 4, a bijection onto [0, G / NSHARD).
     const int b = (int)blockIdx.x;
-    int tile = ((b >> 5) << 5) + ((b & 7) << 2) + ((b >> 3) & 3);
-    const int n = *a.count;
+    const int shard = (b >> 3) % NSHARD;
+    const int GS = G / NSHARD;                   // workgroups per segment
+    const int32_t* seg = a.list + (size_t)shard * a.cap;
+    const int hb = (b >> 3) / NSHARD;
+    int tile = ((hb >> 2) << 5) + ((b & 7) << 2) + (hb & 3);
+    const int n = a.count[shard * CSTRIDE];
     int e = tile * 16 + cl;
     // loads are unconditional, from clamped (always valid) addresses, with the
     // result selected afterwards: a load inside a divergent branch makes the
     // compiler drain every outstanding load at the branch's end
-    int qspec = a.list[min(e, a.cap - 1)];
+    int qspec = seg[min(e, a.cap - 1)];
 
     if (a.cum_dst && b == 0)
         for (int i = (int)threadIdx.x; i < a.n_cum; i += (int)blockDim.x) a.cum_dst[i] += a.cum_src[i];
@@ -84,29 +96,30 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
         const int q = vrow ? qspec : 0;
         const int qr = q / a.Wout, qc = q - (q / a.Wout) * a.Wout;
 
-        // index-map lookups of the 9 input taps, all in flight together
-        uint64_t ev[9];
+        // change stamps of the 9 input taps, all in flight together
+        uint32_t ev[9];
+        int cell[9];
         bool inb[9];
 #pragma unroll
         for (int t = 0; t < 9; ++t) {
             const int ir = S * qr + t / 3 - 1, ic = S * qc + t % 3 - 1;
             inb[t] = vrow && ir >= 0 && ir < a.Hin && ic >= 0 && ic < a.Win;
-            const int irc = min(max(ir, 0), a.Hin - 1), icc = min(max(ic, 0), a.Win - 1);
-            ev[t] = a.map_in[irc * a.Win + icc];
+            cell[t] = min(max(ir, 0), a.Hin - 1) * a.Win + min(max(ic, 0), a.Win - 1);
+            ev[t] = a.stamp_in[cell[t]];
         }
         float* zrow = a.Z + (size_t)q * COUT;
         f4v zo[NCB];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) zo[cb] = *reinterpret_cast<const f4v*>(zrow + (wave * NCB + cb) * 16 + 4 * g);
         // next layer's change list: stamp the footprint in the same round trip
-        // as the index-map and map loads, append the new cells at the end
+        // as the stamp and map loads, append the new cells at the end
         PropBatch<4> pb;
-        if (do_prop) prop_issue<4, true>(a.next, q, vrow, g, a.epoch, pb);
+        if (do_prop) prop_issue<4, false>(a.next, q, vrow, g, a.epoch, pb);
         int rows[9];
         bool any[9];
 #pragma unroll
         for (int t = 0; t < 9; ++t) {
-            rows[t] = (inb[t] && (uint32_t)(ev[t] >> 32) == a.epoch) ? (int)(uint32_t)ev[t] : -1;
+            rows[t] = (inb[t] && ev[t] == a.epoch) ? cell[t] : -1;
             any[t] = __ballot(rows[t] >= 0) != 0ull;    // no changed input under this tap: skip it
         }
 
@@ -199,7 +212,7 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
                         yo.x = fmaxf(yo.x, 0.f); yo.y = fmaxf(yo.y, 0.f); yo.z = fmaxf(yo.z, 0.f); yo.w = fmaxf(yo.w, 0.f);
                         yn.x = fmaxf(yn.x, 0.f); yn.y = fmaxf(yn.y, 0.f); yn.z = fmaxf(yn.z, 0.f); yn.w = fmaxf(yn.w, 0.f);
                     }
-                    char* drow = static_cast<char*>(a.delta_out) + (size_t)e * ROWB_OUT;
+                    char* drow = static_cast<char*>(a.delta_out) + (size_t)q * ROWB_OUT;
                     if constexpr (BF16) {
                         uint2 pn, po;
                         pn.x = f32_to_bf16_bits(yn.x) | (f32_to_bf16_bits(yn.y) << 16);
@@ -219,12 +232,12 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
                 }
             }
         }
-        if (do_prop) prop_finish<4>(a.next, a.epoch, pb);
+        if (do_prop) prop_finish<4>(a.next, a.epoch, shard, pb);
 
-        tile += G;
+        tile += GS;
         e = tile * 16 + cl;
         if (tile * 16 >= n) break;
-        qspec = a.list[min(e, a.cap - 1)];
+        qspec = seg[min(e, a.cap - 1)];
     }
 }
 
@@ -245,7 +258,8 @@ bool layer_supported(int cin, int cout, int stride, bool /*bf16*/) {
 }
 
 hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, int grid, hipStream_t s) {
-    grid = grid < 32 ? 32 : (grid & ~31);   // the first-tile mapping needs a multiple of 32
+    // whole runs of 4 tiles on every XCD for every segment
+    grid = std::max(32 * NSHARD, grid / (32 * NSHARD) * (32 * NSHARD));
 #define SSC_LAUNCH(CI, CO, S)                                                                               \
     if (cin == CI && cout == CO && stride == S) {                                                           \
         dim3 blk(64 * LayerShape<CO>::NW);                                                                  \

@@ -7,18 +7,29 @@
 
 namespace ssc {
 
+// Change sets.  A cell q of a grid belongs to the current stride's set when
+// stamp[q] == epoch; bumping the epoch empties every set at once.
+// Delta rows are stored at their cell's position (a consumer checks the stamp
+// before it gathers a row, so stale rows are never read).  The output sets of
+// the layers are also compacted into lists, the work lists of the layer
+// kernels.  A list is NSHARD segments, each with its own counter, filled by
+// the workgroups b with b % NSHARD == shard: on gfx950 every device-scope
+// atomic executes beyond the per-XCD L2, and appends of all workgroups to one
+// counter queue on that one address.  Workgroup b runs on XCD b % 8.
+constexpr int NSHARD = 2;
+// Distance between the counters of two segments (in int32): one 128-byte line
+// each, since atomics on different words of one line still queue together.
+constexpr int CSTRIDE = 32;
+
 // Change-list propagation target: the next layer's grid and its list state.
-// A cell q of the target grid belongs to the current stride's list when
-// stamp[q] == epoch; map[q] = (epoch << 32) | position of q in `list`.
 struct PropTarget {
     int stride;           // stride of the layer that consumes this list
     int Hin, Win;         // grid the changed cells live in
     int Hout, Wout;       // grid of the target list
     uint32_t* stamp;      // [Hout*Wout]
-    uint64_t* map;        // [Hout*Wout]
-    int32_t* list;        // [Hout*Wout]
-    int32_t* count;       // device counter of the target list
-    int32_t* pairs;       // device counter of (input, output) pairs of the consuming layer
+    int32_t* list;        // NSHARD segments of Hout*Wout entries
+    int32_t* count;       // segment lengths, segment k at count[k * CSTRIDE]
+    int32_t* pairs;       // (input, output) pairs of the consuming layer, same layout
 };
 
 // Changed-cell detection on the input canvas.
@@ -29,11 +40,12 @@ struct DetectArgs {
     const int32_t* prev;  // previous stride's cell list (vanish mode; nullptr: all cells)
     int32_t* prev_out;    // copy of this stride's cell list (present mode, may be nullptr)
     void* X;              // persistent canvas [H0*W0][row bytes]
-    uint32_t* pres;       // presence stamps [H0*W0]
-    uint64_t* map0;       // (epoch << 32) | row in A_0
-    int32_t* list0;       // A_0
-    int32_t* count0;      // |A_0| counter
-    void* delta0;         // packed input deltas in A_0 order
+    uint64_t* pres;       // presence words [H0*W0]: (epoch << 32) | row of the pillar in this stride's list
+    const int32_t* chk_idx;   // vanish mode: this stride's pillar list, checked for duplicate cells (may be nullptr)
+    int32_t chk_count;
+    uint32_t* stamp0;     // change stamps of the input grid [H0*W0]
+    int32_t* count0;      // |A_0| counters, shard k at count0[k * CSTRIDE]
+    void* delta0;         // input deltas, dense by cell [H0*W0][4*C0 bytes]
     int32_t* zero_ptr;    // counters to clear for the next stride (may be nullptr)
     int32_t zero_n;
     int32_t HW;
@@ -42,26 +54,26 @@ struct DetectArgs {
     PropTarget next;
 };
 
-// One convolution layer: contraction of the packed input deltas with the
-// weights, update of the persistent pre-activation map, activation delta
-// epilogue and propagation of the change list to the next layer.
+// One convolution layer: contraction of the input deltas with the weights,
+// update of the persistent pre-activation map, activation delta epilogue and
+// propagation of the change list to the next layer.
 struct LayerArgs {
-    const int32_t* list;      // A_l (cells of the output grid)
-    const int32_t* count;     // |A_l|
-    int cap;                  // capacity of `list` (cells of the output grid)
-    const uint64_t* map_in;   // index map of A_{l-1} on the input grid
-    const void* delta_in;     // packed deltas of layer l-1 in A_{l-1} order
-    const void* wpack;        // weights repacked for the MFMA operand layout
-    float* Z;                 // persistent pre-activation map [Hout*Wout][cout]
-    void* delta_out;          // packed deltas of layer l in A_l order (nullptr: last layer)
+    const int32_t* list;        // A_l: NSHARD segments of `cap` cells of the output grid
+    const int32_t* count;       // segment lengths, segment k at count[k * CSTRIDE]
+    int cap;                    // capacity of a segment (cells of the output grid)
+    const uint32_t* stamp_in;   // change stamps of the input grid [Hin*Win]
+    const void* delta_in;       // input deltas, dense by cell [Hin*Win][4*cin bytes]
+    const void* wpack;          // weights repacked for the MFMA operand layout
+    float* Z;                   // persistent pre-activation map [Hout*Wout][cout]
+    void* delta_out;            // output deltas, dense by cell (nullptr: last layer)
     int Hin, Win, Hout, Wout;
     int relu;
     uint32_t epoch;
     int has_next;
     PropTarget next;
     // running totals, folded in by the last layer of a stride
-    const int32_t* cum_src;   // this stride's counters [n_cum]
-    long long* cum_dst;       // totals [n_cum]
+    const int32_t* cum_src;     // this stride's counters [n_cum]
+    long long* cum_dst;         // totals [n_cum]
     int n_cum;
 };
 
