@@ -70,9 +70,11 @@ enum {
 
 typedef enum { SSCATER_F32 = 0, SSCATER_BF16 = 1 } sscater_dtype;
 
-/* Input grid.  C0 is the pillar feature width.  max_pillars bounds the pillar
- * count of one stride (the paper's pillar budget P with an assertion instead
- * of random sampling, Sec. III-B). */
+/* Input grid: H rows, W columns, each below 32768 and H*W at most 2^30.
+ * C0 is the pillar feature width (C0 * element size a power of two between 16
+ * and 1024 bytes).  max_pillars bounds the pillar count of one stride (the
+ * paper's pillar budget P with an assertion instead of random sampling,
+ * Sec. III-B). */
 typedef struct {
     int32_t H, W, C0, max_pillars;
     int32_t dtype; /* sscater_dtype */

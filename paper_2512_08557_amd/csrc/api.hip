@@ -201,6 +201,7 @@ int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_
     if (!grid || !layers || !weights || !out) return SSCATER_E_INVALID_ARG;
     *out = nullptr;
     if (grid->H <= 0 || grid->W <= 0 || grid->C0 <= 0 || grid->max_pillars < 0) return SSCATER_E_INVALID_ARG;
+    if (grid->H >= 32768 || grid->W >= 32768) return SSCATER_E_INVALID_ARG;   // cell coordinates fit 15 bits
     if (grid->dtype != SSCATER_F32 && grid->dtype != SSCATER_BF16) return SSCATER_E_INVALID_ARG;
     if (n_layers < 1 || n_layers > SSCATER_MAX_LAYERS) return SSCATER_E_INVALID_ARG;
     const bool bf16 = grid->dtype == SSCATER_BF16;

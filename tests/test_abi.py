@@ -49,7 +49,7 @@ def _create(grid, layers, weights=True):
 
 @pytest.mark.parametrize("case", [
     "null_grid", "no_layers", "k5", "pad0", "stride3", "chain", "unsupported_cout", "bad_c0", "bad_dtype",
-    "relu2", "too_many_layers", "huge_grid", "null_weights"])
+    "relu2", "too_many_layers", "huge_grid", "tall_grid", "null_weights"])
 def test_create_rejects_invalid_arguments(case):
     g = E.Grid(32, 32, 64, 100, E.F32)
     L = [E.Layer(64, 64, 3, 2, 1, 1), E.Layer(64, 64, 3, 1, 1, 1)]
@@ -78,6 +78,8 @@ def test_create_rejects_invalid_arguments(case):
         L = [E.Layer(64, 64, 3, 1, 1, 1)] * 33
     elif case == "huge_grid":
         g.H, g.W = 1 << 16, 1 << 16
+    elif case == "tall_grid":               # 32768 x 1 cells is small, but a coordinate needs 16 bits
+        g.H, g.W = 1 << 15, 1
     elif case == "null_weights":
         weights = False
     assert _create(g, L, weights) == ssc.E_INVALID_ARG
