@@ -53,6 +53,62 @@ struct LayerShape {
     static constexpr int NCB = NCBT / NW;                   // cout blocks per wavefront
 };
 
+// One 16-channel (fp32) or 32-value (bf16 pair) chunk of the contraction for
+// NCB output blocks: D[cb] += W_cb^T . dY^T.
+template <bool BF16, int NCB>
+__device__ __forceinline__ void mfma_chunk(f4v (&acc)[NCB], const uint4 av, const uint4 (&bv)[NCB]) {
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+        if constexpr (BF16) {
+            bf8v A, B;
+            __builtin_memcpy(&A, &bv[cb], 16);
+            __builtin_memcpy(&B, &av, 16);
+            acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B, acc[cb], 0, 0, 0);
+        } else {
+            acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bv[cb].x), __uint_as_float(av.x), acc[cb], 0, 0, 0);
+            acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bv[cb].y), __uint_as_float(av.y), acc[cb], 0, 0, 0);
+            acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bv[cb].z), __uint_as_float(av.z), acc[cb], 0, 0, 0);
+            acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bv[cb].w), __uint_as_float(av.w), acc[cb], 0, 0, 0);
+        }
+    }
+}
+
+// Z update and next-layer delta row of one lane: output cell q, output
+// channels co0 .. co0+3 (fp32 Z_new = Z_old + D; delta phi(Z_new) -
+// phi(Z_old), or the bf16 pair [bf16(phi(Z_new)) | bf16(phi(Z_old))]).
+template <int COUT, bool BF16>
+__device__ __forceinline__ void epilogue4(const LayerArgs& a, int q, int co0, const f4v o, const f4v d) {
+    f4v zn;
+    zn.x = o.x + d.x;
+    zn.y = o.y + d.y;
+    zn.z = o.z + d.z;
+    zn.w = o.w + d.w;
+    *reinterpret_cast<f4v*>(a.Z + (size_t)q * COUT + co0) = zn;
+    if (!a.delta_out) return;
+    f4v yo = o, yn = zn;
+    if (a.relu) {
+        yo.x = fmaxf(yo.x, 0.f); yo.y = fmaxf(yo.y, 0.f); yo.z = fmaxf(yo.z, 0.f); yo.w = fmaxf(yo.w, 0.f);
+        yn.x = fmaxf(yn.x, 0.f); yn.y = fmaxf(yn.y, 0.f); yn.z = fmaxf(yn.z, 0.f); yn.w = fmaxf(yn.w, 0.f);
+    }
+    char* drow = static_cast<char*>(a.delta_out) + (size_t)q * (4 * COUT);
+    if constexpr (BF16) {
+        uint2 pn, po;
+        pn.x = f32_to_bf16_bits(yn.x) | (f32_to_bf16_bits(yn.y) << 16);
+        pn.y = f32_to_bf16_bits(yn.z) | (f32_to_bf16_bits(yn.w) << 16);
+        po.x = f32_to_bf16_bits(yo.x) | (f32_to_bf16_bits(yo.y) << 16);
+        po.y = f32_to_bf16_bits(yo.z) | (f32_to_bf16_bits(yo.w) << 16);
+        *reinterpret_cast<uint2*>(drow + co0 * 2) = pn;
+        *reinterpret_cast<uint2*>(drow + COUT * 2 + co0 * 2) = po;
+    } else {
+        f4v dy;
+        dy.x = yn.x - yo.x;
+        dy.y = yn.y - yo.y;
+        dy.z = yn.z - yo.z;
+        dy.w = yn.w - yo.w;
+        *reinterpret_cast<f4v*>(drow + co0 * 4) = dy;
+    }
+}
+
 template <int CIN, int COUT, int S, bool BF16>
 __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerArgs a) {
     constexpr int NCBT = LayerShape<COUT>::NCBT;
@@ -197,40 +253,7 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
 
         if (vrow) {
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) {
-                const int co0 = (wave * NCB + cb) * 16 + 4 * g;
-                const f4v o = zo[cb];
-                f4v zn;
-                zn.x = o.x + acc[cb].x;
-                zn.y = o.y + acc[cb].y;
-                zn.z = o.z + acc[cb].z;
-                zn.w = o.w + acc[cb].w;
-                *reinterpret_cast<f4v*>(zrow + co0) = zn;
-                if (a.delta_out) {
-                    f4v yo = o, yn = zn;
-                    if (a.relu) {
-                        yo.x = fmaxf(yo.x, 0.f); yo.y = fmaxf(yo.y, 0.f); yo.z = fmaxf(yo.z, 0.f); yo.w = fmaxf(yo.w, 0.f);
-                        yn.x = fmaxf(yn.x, 0.f); yn.y = fmaxf(yn.y, 0.f); yn.z = fmaxf(yn.z, 0.f); yn.w = fmaxf(yn.w, 0.f);
-                    }
-                    char* drow = static_cast<char*>(a.delta_out) + (size_t)q * ROWB_OUT;
-                    if constexpr (BF16) {
-                        uint2 pn, po;
-                        pn.x = f32_to_bf16_bits(yn.x) | (f32_to_bf16_bits(yn.y) << 16);
-                        pn.y = f32_to_bf16_bits(yn.z) | (f32_to_bf16_bits(yn.w) << 16);
-                        po.x = f32_to_bf16_bits(yo.x) | (f32_to_bf16_bits(yo.y) << 16);
-                        po.y = f32_to_bf16_bits(yo.z) | (f32_to_bf16_bits(yo.w) << 16);
-                        *reinterpret_cast<uint2*>(drow + co0 * 2) = pn;
-                        *reinterpret_cast<uint2*>(drow + COUT * 2 + co0 * 2) = po;
-                    } else {
-                        f4v dy;
-                        dy.x = yn.x - yo.x;
-                        dy.y = yn.y - yo.y;
-                        dy.z = yn.z - yo.z;
-                        dy.w = yn.w - yo.w;
-                        *reinterpret_cast<f4v*>(drow + co0 * 4) = dy;
-                    }
-                }
-            }
+            for (int cb = 0; cb < NCB; ++cb) epilogue4<COUT, BF16>(a, q, (wave * NCB + cb) * 16 + 4 * g, zo[cb], acc[cb]);
         }
         if (do_prop) prop_finish<4>(a.next, a.epoch, shard, pb);
 
@@ -239,6 +262,125 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
         if (tile * 16 >= n) break;
         qspec = seg[min(e, a.cap - 1)];
     }
+}
+
+
+// ---------------------------------------------------------------------------
+// wide layers (more than 4 chunks of 16 input channels per tap)
+// ---------------------------------------------------------------------------
+// Here one tile's weights (9 * cin * cout values) are far larger than its
+// deltas, so a workgroup covers 2 tiles x 2 output-channel blocks (4
+// wavefronts, one tile and one block each; the cout dimension is spread over
+// NCBT/2 workgroups) and streams both operands tap by tap through LDS with
+// asynchronous global->LDS copies, double-buffered: while the matrix cores
+// work on tap t from registers, the copies of the next tap are in flight.
+// Each copy is shared by the two wavefronts that need it (a vector load of the
+// same bytes by every wavefront costs several times more per compute unit).
+// Stage layout: [slot][chunk][lane] with slots tile 0, tile 1, block 0,
+// block 1; lane l of a 16-byte-per-lane copy lands at base + 16*l, which is
+// the MFMA operand layout.  Taps without a changed input in either tile are
+// skipped by the whole workgroup.
+template <int CIN, int COUT, bool BF16>
+struct WideShape {
+    static constexpr int KTOT = BF16 ? 2 * CIN : CIN;
+    static constexpr int NCH = KTOT / (BF16 ? 32 : 16);    // 1 KB operand chunks per tap
+    static constexpr int NCBT = COUT / 16;
+    static constexpr int NH = NCBT / 2;                     // workgroups per tile pair
+};
+
+template <int CIN, int COUT, int S, bool BF16>
+__global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
+    using W = WideShape<CIN, COUT, BF16>;
+    constexpr int NCH = W::NCH, NCBT = W::NCBT, NH = W::NH;
+    constexpr int ROWB_IN = 4 * CIN;
+    static_assert(NCH % 2 == 0 && NCBT % 2 == 0, "shape");
+    __shared__ uint4 stage[2][4][NCH][64];
+    __shared__ int tapmask;
+
+    const int lane = (int)(threadIdx.x & 63u), wave = (int)(threadIdx.x >> 6);
+    const int cl = lane & 15, g = lane >> 4;
+    const int tp = wave & 1, cbl = wave >> 1;          // tile and cout block of this wavefront
+    const int b = (int)blockIdx.x;
+    const int h = b % NH;                              // cout blocks 2h, 2h+1
+    const int shard = (b / NH) % NSHARD;
+    const int GL = (int)gridDim.x / (NH * NSHARD);     // workgroups per (segment, cout group)
+    const int32_t* seg = a.list + (size_t)shard * a.cap;
+    const int n = a.count[shard * CSTRIDE];
+    const int cbg = 2 * h + cbl;                       // global cout block of this wavefront
+    const bool do_prop = a.has_next && h == 0 && cbl == 0;
+    const char* dbase = static_cast<const char*>(a.delta_in) + g * 16;
+    const uint4* wbase = static_cast<const uint4*>(a.wpack) + lane;
+
+    for (int pair = (b / NH) / NSHARD; pair * 32 < n; pair += GL) {
+        const int e = (2 * pair + tp) * 16 + cl;
+        const bool vrow = e < n;
+        const int q = vrow ? seg[min(e, a.cap - 1)] : 0;
+        const int qr = q / a.Wout, qc = q - (q / a.Wout) * a.Wout;
+        int rows[9];
+        unsigned mask = 0u;
+#pragma unroll
+        for (int t = 0; t < 9; ++t) {
+            const int ir = S * qr + t / 3 - 1, ic = S * qc + t % 3 - 1;
+            const bool inb = vrow && ir >= 0 && ir < a.Hin && ic >= 0 && ic < a.Win;
+            const int cell = min(max(ir, 0), a.Hin - 1) * a.Win + min(max(ic, 0), a.Win - 1);
+            rows[t] = (inb && a.stamp_in[cell] == a.epoch) ? cell : -1;
+            if (__ballot(rows[t] >= 0) != 0ull) mask |= 1u << t;
+        }
+        const f4v zo = *reinterpret_cast<const f4v*>(a.Z + (size_t)q * COUT + cbg * 16 + 4 * g);
+        PropBatch<4> pb;
+        if (do_prop) prop_issue<4, false>(a.next, q, vrow, g, a.epoch, pb);
+        if (threadIdx.x == 0) tapmask = 0;
+        __syncthreads();
+        if (lane == 0 && mask) atomicOr(&tapmask, (int)mask);
+        __syncthreads();
+        unsigned taps = (unsigned)tapmask;
+
+        // copies of tap t into buffer bi: the two wavefronts of a tile share
+        // its delta chunks, the two wavefronts of a cout block its weights
+        auto issue = [&](int t, int bi) __attribute__((always_inline)) {
+            const int row = max(rows[t], 0);
+#pragma unroll
+            for (int c = cbl; c < NCH; c += 2)
+                __builtin_amdgcn_global_load_lds(
+                    (const __attribute__((address_space(1))) void*)(dbase + (size_t)row * ROWB_IN + c * 64),
+                    (__attribute__((address_space(3))) void*)&stage[bi][tp][c][0], 16, 0, 0);
+#pragma unroll
+            for (int c = tp; c < NCH; c += 2)
+                __builtin_amdgcn_global_load_lds(
+                    (const __attribute__((address_space(1))) void*)(wbase + ((size_t)(t * NCH + c) * NCBT + cbg) * 64),
+                    (__attribute__((address_space(3))) void*)&stage[bi][2 + cbl][c][0], 16, 0, 0);
+        };
+
+        f4v acc[1] = {f4v{0.f, 0.f, 0.f, 0.f}};
+        int bi = 0;
+        if (taps) issue(__builtin_ctz(taps), 0);
+        while (taps) {
+            const int t = __builtin_ctz(taps);
+            taps &= taps - 1u;
+            __builtin_amdgcn_s_waitcnt(0);             // this wavefront's copies of tap t
+            __syncthreads();                           // everyone's copies of tap t; buffer bi^1 is free
+            uint4 av[NCH], bv[NCH];
+            const uint32_t m = rows[t] >= 0 ? ~0u : 0u;   // unchanged input: zero row
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+                const uint4 x = stage[bi][tp][c][lane];
+                av[c] = make_uint4(x.x & m, x.y & m, x.z & m, x.w & m);
+                bv[c] = stage[bi][2 + cbl][c][lane];
+            }
+            if (taps) issue(__builtin_ctz(taps), bi ^ 1);
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+                const uint4 bb[1] = {bv[c]};
+                mfma_chunk<BF16, 1>(acc, av[c], bb);
+            }
+            bi ^= 1;
+        }
+        if (vrow) epilogue4<COUT, BF16>(a, q, cbg * 16 + 4 * g, zo, acc[0]);
+        if (do_prop) prop_finish<4>(a.next, a.epoch, shard, pb);
+        __syncthreads();                               // the stage buffers are free again
+    }
+    if (a.cum_dst && b == 0)
+        for (int i = (int)threadIdx.x; i < a.n_cum; i += (int)blockDim.x) a.cum_dst[i] += a.cum_src[i];
 }
 
 // ---------------------------------------------------------------------------
@@ -257,16 +399,26 @@ bool layer_supported(int cin, int cout, int stride, bool /*bf16*/) {
     return false;
 }
 
-hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, int grid, hipStream_t s) {
-    // whole runs of 4 tiles on every XCD for every segment
-    grid = std::max(32 * NSHARD, grid / (32 * NSHARD) * (32 * NSHARD));
-#define SSC_LAUNCH(CI, CO, S)                                                                               \
-    if (cin == CI && cout == CO && stride == S) {                                                           \
-        dim3 blk(64 * LayerShape<CO>::NW);                                                                  \
-        if (bf16) hipLaunchKernelGGL((layer_kernel<CI, CO, S, true>), dim3(grid), blk, 0, s, a);             \
-        else hipLaunchKernelGGL((layer_kernel<CI, CO, S, false>), dim3(grid), blk, 0, s, a);                 \
-        return hipGetLastError();                                                                           \
+template <int CI, int CO, int S, bool BF16>
+static hipError_t launch_shape(const LayerArgs& a, int grid, hipStream_t s) {
+    if constexpr (WideShape<CI, CO, BF16>::NCH > 4 && CO >= 32) {
+        // tile pairs x cout groups x segments; at most ceil(cap / 32) pairs per segment
+        constexpr int NH = WideShape<CI, CO, BF16>::NH;
+        int gl = std::max(1, grid / (2 * NH * NSHARD));
+        gl = std::min(gl, std::max(1, (a.cap + 31) / 32));
+        hipLaunchKernelGGL((layer_kernel_wide<CI, CO, S, BF16>), dim3(gl * NH * NSHARD), dim3(256), 0, s, a);
+    } else {
+        // whole runs of 4 tiles on every XCD for every segment
+        grid = std::max(32 * NSHARD, grid / (32 * NSHARD) * (32 * NSHARD));
+        hipLaunchKernelGGL((layer_kernel<CI, CO, S, BF16>), dim3(grid), dim3(64 * LayerShape<CO>::NW), 0, s, a);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, int grid, hipStream_t s) {
+#define SSC_LAUNCH(CI, CO, S)                                                                               \
+    if (cin == CI && cout == CO && stride == S)                                                             \
+        return bf16 ? launch_shape<CI, CO, S, true>(a, grid, s) : launch_shape<CI, CO, S, false>(a, grid, s);
     SSC_ALL_SHAPES(SSC_LAUNCH)
 #undef SSC_LAUNCH
     return hipErrorInvalidValue;

@@ -77,7 +77,7 @@ def _block(cin: int, f: int, n: int) -> List[LayerSpec]:
 _BACKBONE = tuple(_block(64, 64, 4) + _block(64, 128, 6) + _block(128, 256, 6))
 
 WORKLOADS = {
-    "c1": Workload("c1", 64, 64, 16, "f32", (LayerSpec(16, 16, 1, False),), 10, 1024,
+    "c1": Workload("c1", 64, 64, 16, "f32", (LayerSpec(16, 16, 1, False),), 10, 4096,
                    "single 3x3 s1 conv 16->16, 64x64 grid, no ReLU"),
     "c2": Workload("c2", 496, 432, 64, "f32", tuple(_block(64, 64, 4)), 100, 16000,
                    "PointPillars block 1 (s2 + 3 x s1, 64 ch, ReLU) on 432x496"),
