@@ -364,26 +364,47 @@ def main() -> int:
                 k["bytes"] += (act2[l - 1] * sp.cin * e_d + act2[l] * sp.cout * 8.0 +
                                (act2[l] * sp.cout * e_d if l < L else 0.0) +
                                cnt[slot] * 9.0 * sp.cin * sp.cout * (2 if wl.dtype == "bf16" else 4) +
-                               12.0 * (act2[l - 1] + act2[l]))
+                               8.0 * (act2[l - 1] + act2[l]))
+        # an event pair with nothing between it, on the same stream: the part of
+        # an event-bracketed launch that is not the kernel itself
+        pair_ms = []
+        for _ in range(3):
+            evp = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(64)]
+            torch.cuda.synchronize()
+            for e0, e1 in evp:
+                e0.record(stream)
+                e1.record(stream)
+            torch.cuda.synchronize()
+            pair_ms.append(statistics.median(e0.elapsed_time(e1) for e0, e1 in evp))
+        pair_us = min(pair_ms) * 1e3
         for name, k in kernels.items():
             log(f"[bench] {name:34s} {k['launches']:5d} launches  avg {k['ms'] / k['launches'] * 1e3:8.2f} us  "
                 f"total {k['ms']:.3f} ms")
+        log(f"[bench] empty event pair on the stream: {pair_us:.2f} us")
         dom_name, dom = max(kernels.items(), key=lambda kv: kv[1]["ms"])
         if dom["flops"] > 0:
+            # the event-bracketed duration includes the dispatch of the kernel and
+            # the two timestamp packets (conservative: it only lowers `achieved`)
+            launch_us = dom["ms"] / dom["launches"] * 1e3
+            secs = launch_us * 1e-6 * dom["launches"]
             intensity = dom["flops"] / max(dom["bytes"], 1.0)
             peak_t = PEAK_TFLOPS[wl.dtype]
+            traffic = read_traffic(dom_name, wl.name)
             if intensity >= peak_t * 1e12 / (PEAK_HBM_GBS * 1e9):
-                achieved = dom["flops"] / (dom["ms"] / 1e3) / 1e12
+                achieved = dom["flops"] / secs / 1e12
                 roofline = {"bound": "mfma", "achieved": achieved, "peak": peak_t, "unit": "TFLOP/s",
-                            "frac": achieved / peak_t, "traffic": None}
+                            "frac": achieved / peak_t, "traffic": traffic}
             else:
-                achieved = dom["bytes"] / (dom["ms"] / 1e3) / 1e9
+                achieved = dom["bytes"] / secs / 1e9
                 roofline = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                            "frac": achieved / PEAK_HBM_GBS, "traffic": None}
+                            "frac": achieved / PEAK_HBM_GBS, "traffic": traffic}
             roofline.update({"kernel": dom_name, "launches": dom["launches"],
-                             "avg_launch_us": dom["ms"] / dom["launches"] * 1e3,
+                             "avg_launch_us": launch_us,
+                             "empty_event_pair_us": pair_us,
                              "alg_flops_per_launch": dom["flops"] / dom["launches"],
-                             "alg_bytes_per_launch": dom["bytes"] / dom["launches"]})
+                             "alg_bytes_per_launch": dom["bytes"] / dom["launches"],
+                             "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
+                                             "scaled by a plain copy)"})
 
     # ---- GPU full recompute: reset + full window through the same kernels ----
     full = []
