@@ -109,15 +109,18 @@ def cpu_baseline(wl, ws, strides, first, budget_s):
 # HBM traffic of the dominant kernel from --pmc FETCH_SIZE / WRITE_SIZE runs
 # scaled by what the same counters read for a plain copy of known size.
 # --------------------------------------------------------------------------
+KERNEL_SOURCES = ("detect.hip", "layer.hip", "misc.hip", "device_common.h", "sscater_internal.h")
+
+
 def kernel_source_digest() -> str:
-    """sha256 over the library's kernel sources: a measured traffic figure is
-    only reported while the kernels are the ones it was measured on."""
+    """sha256 over the device-code sources (not the host-side API): a measured
+    traffic figure is only reported while the kernels are the ones it was
+    measured on."""
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2512_08557_amd", "csrc", "*"))):
-        if f.endswith((".hip", ".h")):
-            h.update(os.path.basename(f).encode())
-            with open(f, "rb") as fh:
-                h.update(fh.read())
+    for name in KERNEL_SOURCES:
+        h.update(name.encode())
+        with open(os.path.join(ROOT, "paper_2512_08557_amd", "csrc", name), "rb") as fh:
+            h.update(fh.read())
     return h.hexdigest()
 
 

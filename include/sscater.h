@@ -119,8 +119,8 @@ typedef struct sscater* sscater_t;
  *   weights[l] : host pointer to layer l's OIHW weights [cout][cin][3][3] in the
  *                grid dtype; copied and repacked, so the caller may free them
  *                on return.
- * All state (input canvas, per-layer pre-activation maps, change lists, index
- * maps, delta buffers) is allocated here, sized for the worst case; no later
+ * All state (input canvas, per-layer pre-activation maps, change lists, change
+ * stamps, delta buffers) is allocated here, sized for the worst case; no later
  * call allocates.  The maps start at zero (an empty window). */
 int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
                    const void* const* weights, sscater_t* out);

@@ -2,9 +2,10 @@
 // allocation, weight repacking and the per-stride launch sequence.
 //
 // Per stride, on the caller's stream, with no host synchronisation:
-//   1. detect (present)  : new pillars vs canvas -> A_0, packed input deltas,
+//   1. detect (present)  : new pillars vs canvas -> A_0 stamps, input deltas,
 //                          canvas update, A_0 -> A_1 propagation;
-//   2. detect (vanished) : previous list minus the new list -> same outputs;
+//   2. detect (vanished) : previous list minus the new list -> same outputs,
+//                          and the duplicate check of the new list;
 //   3. layer l = 1..L    : contraction over A_l, Z_l update, delta epilogue,
 //                          A_l -> A_{l+1} propagation.
 // Work sizes live in device counters; the layer kernels walk their tiles from
