@@ -19,6 +19,11 @@ What it computes (SSCATeR, arXiv 2512.08557):
   the scatter of a changed site is marked, and for stride > 1 a downsampled
   site is marked when any site under its kernel is changed).  The GPU path
   builds the same sets in the scatter direction.
+* ``conv_transpose`` / ``forward_neck`` / ``upsample_mask``: the neck that
+  upsamples block outputs by a transposed convolution with kernel = stride and
+  concatenates them (Sec. III-B, backbone paragraph).  Upsampled change sets
+  follow Alg. 1's deconvolution rule: every upsampled site under a changed
+  site is changed.
 * ``value_changed``: the cells whose layer output value actually differs
   between two windows (used for the locality invariant: a value can only change
   where the structural set says so).
@@ -57,6 +62,9 @@ def _load():
                                             ip, ip, ip, ip, ctypes.POINTER(dp), ctypes.c_int,
                                             ctypes.POINTER(dp)]
         lib.oracle_backbone_f64.restype = ctypes.c_int
+        lib.oracle_convT_f64.argtypes = [dp, ctypes.c_int, ctypes.c_int, ctypes.c_int, dp,
+                                         ctypes.c_int, ctypes.c_int, dp]
+        lib.oracle_convT_f64.restype = ctypes.c_int
         lib.oracle_threads.argtypes = []
         lib.oracle_threads.restype = ctypes.c_int
         _lib = lib
@@ -124,6 +132,63 @@ def forward(x0: np.ndarray, weights: Sequence[np.ndarray], layers: Sequence[Tupl
     if rc != 0:
         raise ValueError("oracle_backbone_f64 rejected its arguments")
     return ys
+
+
+def conv_transpose(x: np.ndarray, w: np.ndarray, stride: int) -> np.ndarray:
+    """Transposed conv, kernel = stride, no padding. x: [H, W, cin] float64;
+    w: [cin, cout, s, s] (ConvTranspose2d layout). Returns [H*s, W*s, cout]."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    w = np.ascontiguousarray(w, dtype=np.float64)
+    H, W, cin = x.shape
+    cout = w.shape[1]
+    assert w.shape == (cin, cout, stride, stride)
+    out = np.empty((H * stride, W * stride, cout), dtype=np.float64)
+    rc = _load().oracle_convT_f64(_dptr(x), H, W, cin, _dptr(w), cout, stride, _dptr(out))
+    if rc != 0:
+        raise ValueError("oracle_convT_f64 rejected its arguments")
+    return out
+
+
+def forward_neck(ys: Sequence[np.ndarray], up_weights: Sequence[np.ndarray],
+                 ups: Sequence[Tuple[int, int, int, bool]], bf16_storage: bool = False) -> np.ndarray:
+    """The neck output: for each upsampler (src_layer 1..L, cout, stride,
+    relu), phi(conv_transpose(Y_src)), bf16-rounded for bf16 storage, all
+    concatenated along the channels in order.  ys: Y_1..Y_L from forward()."""
+    outs = []
+    for (src, _cout, s, relu), w in zip(ups, up_weights):
+        z = conv_transpose(ys[src - 1], w, s)
+        if relu:
+            z = np.maximum(z, 0.0)
+        if bf16_storage:
+            z = round_bf16(z)
+        outs.append(z)
+    shapes = {o.shape[:2] for o in outs}
+    assert len(shapes) == 1, "upsampled maps must share one grid"
+    return np.concatenate(outs, axis=-1)
+
+
+def upsample_mask(mask: np.ndarray, stride: int) -> np.ndarray:
+    """Alg. 1, deconvolution rule: output (y, x) is changed iff its one input
+    cell (y // s, x // s) is changed."""
+    H, W = mask.shape
+    ys = np.arange(H * stride) // stride
+    xs = np.arange(W * stride) // stride
+    return mask[np.ix_(ys, xs)]
+
+
+def neck_changed(lists: Sequence[np.ndarray], layer_shapes: Sequence[Tuple[int, int]],
+                 ups: Sequence[Tuple[int, int, int, bool]]) -> np.ndarray:
+    """Sorted cell list of the neck's change set: the union of the upsampled
+    sets of the source layers.  lists: A_0..A_L as from changed_lists();
+    layer_shapes: (H_l, W_l) for l = 1..L."""
+    out = None
+    for (src, _cout, s, _relu) in ups:
+        H, W = layer_shapes[src - 1]
+        m = np.zeros(H * W, dtype=bool)
+        m[lists[src]] = True
+        up = upsample_mask(m.reshape(H, W), s)
+        out = up if out is None else (out | up)
+    return np.flatnonzero(out)
 
 
 # ---------------------------------------------------------------------------

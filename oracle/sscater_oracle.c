@@ -141,6 +141,40 @@ ORACLE_API int oracle_backbone_f64(const double* x0, int H0, int W0, int C0, int
     return 0;
 }
 
+/*
+ * Transposed convolution with kernel = stride s (the upsampling of the
+ * PointPillars neck that brings every block to a common grid before the
+ * concatenation; Sec. III-B, backbone paragraph, and Alg. 1, deconvolution
+ * branch).  Kernel and stride equal, so every output cell has exactly one
+ * input cell:
+ *   out[s*i + a][s*j + b][co] = sum_ci in[i][j][ci] * w[ci][co][a][b]
+ *   in  : [H][W][cin]; w: [cin][cout][s][s] (the PyTorch ConvTranspose2d
+ *   layout); out : [H*s][W*s][cout].
+ * Returns 0, or -1 on bad arguments.
+ */
+ORACLE_API int oracle_convT_f64(const double* in, int H, int W, int cin, const double* w, int cout, int s,
+                                double* out) {
+    if (!in || !w || !out || H <= 0 || W <= 0 || cin <= 0 || cout <= 0 || s <= 0) return -1;
+    const int Wo = W * s;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int i = 0; i < H; ++i)
+        for (int j = 0; j < W; ++j) {
+            const double* a_in = in + ((size_t)i * W + j) * cin;
+            for (int a = 0; a < s; ++a)
+                for (int b = 0; b < s; ++b) {
+                    double* o = out + ((size_t)(s * i + a) * Wo + (s * j + b)) * cout;
+                    for (int co = 0; co < cout; ++co) o[co] = 0.0;
+                    for (int ci = 0; ci < cin; ++ci) {
+                        const double v = a_in[ci];
+                        if (v == 0.0) continue;
+                        const double* wr = w + (size_t)ci * cout * s * s;
+                        for (int co = 0; co < cout; ++co) o[co] += v * wr[((size_t)co * s + a) * s + b];
+                    }
+                }
+        }
+    return 0;
+}
+
 #ifdef _OPENMP
 #include <omp.h>
 #endif

@@ -37,7 +37,7 @@ SCENE_SEED = 2512
 WEIGHT_SEED = 8557
 
 __all__ = [
-    "LayerSpec", "Workload", "workload", "WORKLOADS", "weights", "make_stream",
+    "LayerSpec", "Workload", "workload", "WORKLOADS", "weights", "make_stream", "UpSpec", "neck", "neck_weights",
     "Stream", "Stride", "round_to_bf16_bits", "bf16_bits_to_f32", "out_shape",
     "cell_azimuth_sector",
 ]
@@ -92,6 +92,42 @@ WORKLOADS = {
 
 def workload(name: str) -> Workload:
     return WORKLOADS[name]
+
+
+@dataclasses.dataclass(frozen=True)
+class UpSpec:
+    """One upsampler of the neck: transposed conv with kernel = stride on the
+    output of backbone layer `src` (1-based), then ReLU."""
+    src: int
+    cout: int
+    stride: int
+    relu: bool
+
+
+# PointPillars neck on the 3-block backbone: every block output upsampled to
+# the first block's 248x216 grid with 128 channels, concatenated (384).
+_NECK = (UpSpec(4, 128, 1, True), UpSpec(10, 128, 2, True), UpSpec(16, 128, 4, True))
+NECKS = {"c3": _NECK, "c4": _NECK}
+
+
+def neck(name: str) -> Tuple[UpSpec, ...]:
+    return NECKS.get(name, ())
+
+
+def neck_weights(name: str) -> List[np.ndarray]:
+    """Per-upsampler [cin, cout, s, s] float32 weights, He-normal N(0, 2/cin)
+    (each output cell sums cin products); bf16-representable for bf16
+    workloads."""
+    wl = workload(name)
+    out = []
+    for u, up in enumerate(neck(name)):
+        cin = wl.layers[up.src - 1].cout
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence((WEIGHT_SEED, 2, 100 + u))))
+        w = (rng.standard_normal((cin, up.cout, up.stride, up.stride)) * math.sqrt(2.0 / cin)).astype(np.float32)
+        if wl.dtype == "bf16":
+            w = bf16_bits_to_f32(round_to_bf16_bits(w)).reshape(w.shape)
+        out.append(np.ascontiguousarray(w))
+    return out
 
 
 def out_shape(H: int, W: int, stride: int) -> Tuple[int, int]:

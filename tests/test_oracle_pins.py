@@ -332,3 +332,101 @@ def test_pair_counts_equal_sum_of_single_cell_footprints(s):
             single.flat[p] = True
             expect += int(oracle.propagate_gather(single, s).sum())
         assert oracle.pair_counts(mask, s) == expect
+
+
+# ------------------------------------------------------------ neck (upsampling + concat)
+@pytest.mark.parametrize("s", [1, 2, 4])
+def test_conv_transpose_matches_torch(s):
+    """Library special case: torch's ConvTranspose2d (kernel = stride, no
+    padding) in float64."""
+    import torch
+    rng = np.random.default_rng(10 + s)
+    x = rng.standard_normal((5, 6, 3))
+    w = rng.standard_normal((3, 4, s, s))
+    got = oracle.conv_transpose(x, w, s)
+    ref = torch.nn.functional.conv_transpose2d(torch.from_numpy(x).permute(2, 0, 1)[None], torch.from_numpy(w),
+                                               stride=s)[0].permute(1, 2, 0).numpy()
+    assert got.shape == (5 * s, 6 * s, 4)
+    assert np.abs(got - ref).max() <= 1e-12 * np.abs(ref).max()
+
+
+def test_conv_transpose_brute_force():
+    """Every output cell is one input cell's row times one kernel position."""
+    rng = np.random.default_rng(3)
+    s, H, W, cin, cout = 2, 3, 2, 2, 3
+    x = rng.standard_normal((H, W, cin))
+    w = rng.standard_normal((cin, cout, s, s))
+    ref = np.zeros((H * s, W * s, cout))
+    for i in range(H):
+        for j in range(W):
+            for a in range(s):
+                for b in range(s):
+                    for co in range(cout):
+                        for ci in range(cin):
+                            ref[s * i + a, s * j + b, co] += x[i, j, ci] * w[ci, co, a, b]
+    assert np.abs(oracle.conv_transpose(x, w, s) - ref).max() <= 1e-13
+
+
+@pytest.mark.parametrize("s", [1, 2, 4])
+def test_upsample_rule_is_the_dependency_of_conv_transpose(s):
+    """Alg. 1, deconvolution branch: perturbing one input cell changes exactly
+    the upsampled sites under it, which upsample_mask names."""
+    rng = np.random.default_rng(20 + s)
+    H, W = 4, 5
+    x = rng.standard_normal((H, W, 2))
+    w = rng.standard_normal((2, 3, s, s))
+    base = oracle.conv_transpose(x, w, s)
+    for (i, j) in [(0, 0), (2, 3), (3, 4)]:
+        y = x.copy()
+        y[i, j] += 1.0
+        diff = np.any(oracle.conv_transpose(y, w, s) != base, axis=-1)
+        m = np.zeros((H, W), dtype=bool)
+        m[i, j] = True
+        np.testing.assert_array_equal(diff, oracle.upsample_mask(m, s))
+        assert diff.sum() == s * s
+
+
+def test_neck_concat_and_union():
+    """The neck output is the channel concatenation of the upsampled maps in
+    order, and its change set is the union of the upsampled sets."""
+    rng = np.random.default_rng(7)
+    # sources on 8x4, 4x2 and 2x1 grids, all upsampled to 8x4
+    ys = [rng.standard_normal((8, 4, 2)), rng.standard_normal((4, 2, 3)), rng.standard_normal((2, 1, 4))]
+    ups = [(1, 2, 1, True), (2, 3, 2, False), (3, 1, 4, True)]
+    ws = [rng.standard_normal((2, 2, 1, 1)), rng.standard_normal((3, 3, 2, 2)), rng.standard_normal((4, 1, 4, 4))]
+    out = oracle.forward_neck(ys, ws, ups)
+    assert out.shape == (8, 4, 6)
+    np.testing.assert_array_equal(out[..., :2], np.maximum(oracle.conv_transpose(ys[0], ws[0], 1), 0))
+    np.testing.assert_array_equal(out[..., 2:5], oracle.conv_transpose(ys[1], ws[1], 2))
+    np.testing.assert_array_equal(out[..., 5:], np.maximum(oracle.conv_transpose(ys[2], ws[2], 4), 0))
+    # A_1 = {0, 31} on 8x4, A_2 = {5} on 4x2 (cell (2, 1)), A_3 = {1} on 2x1 (cell (1, 0))
+    lists = [np.zeros(0, np.int64), np.array([0, 31]), np.array([5]), np.array([1])]
+    got = oracle.neck_changed(lists, [(8, 4), (4, 2), (2, 1)], ups)
+    want = {0, 31}
+    want |= {(2 * 2 + a) * 4 + (2 * 1 + b) for a in range(2) for b in range(2)}
+    want |= {(4 * 1 + a) * 4 + b for a in range(4) for b in range(4)}
+    np.testing.assert_array_equal(got, np.array(sorted(want)))
+
+
+def test_neck_recycling_equals_recompute():
+    """The delta form for the neck: Z_up(new) = Z_up(old) + convT(Y_src(new) -
+    Y_src(old)), with the source delta nonzero only on the source's change set,
+    so updating the upsampled blocks of the changed cells reproduces the
+    recomputed map."""
+    rng = np.random.default_rng(11)
+    w = rng.standard_normal((3, 2, 2, 2))
+    y_old = rng.standard_normal((5, 4, 3))
+    y_new = y_old.copy()
+    changed = [(0, 1), (3, 3), (4, 0)]
+    for (i, j) in changed:
+        y_new[i, j] = rng.standard_normal(3)
+    z = oracle.conv_transpose(y_old, w, 2)
+    d = oracle.conv_transpose(y_new - y_old, w, 2)
+    m = np.zeros((5, 4), dtype=bool)
+    for (i, j) in changed:
+        m[i, j] = True
+    up = oracle.upsample_mask(m, 2)
+    assert not np.any(d[~up])                 # no change outside the upsampled set
+    z[up] += d[up]
+    ref = oracle.conv_transpose(y_new, w, 2)
+    assert np.abs(z - ref).max() <= 1e-12 * np.abs(ref).max()
