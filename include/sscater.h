@@ -58,6 +58,7 @@ extern "C" {
 #endif
 
 #define SSCATER_MAX_LAYERS 32
+#define SSCATER_MAX_UPSAMPLERS 4
 
 enum {
     SSCATER_OK = 0,
@@ -86,6 +87,17 @@ typedef struct {
     int32_t cin, cout, k, stride, pad, relu;
 } sscater_layer;
 
+/* One upsampler of the neck (Sec. III-B, backbone paragraph: every block is
+ * upsampled and the results are concatenated; Alg. 1, deconvolution branch):
+ * a transposed convolution with kernel = stride (1, 2 or 4, no padding) on the
+ * output Y of backbone layer src_layer (1-based), then ReLU if relu = 1.
+ * Output cell (s*i + a, s*j + b) takes exactly input cell (i, j) times
+ * W[:, :, a, b].  All upsamplers of a handle must map onto one grid; their
+ * outputs are concatenated along the channels in order (the neck map). */
+typedef struct {
+    int32_t src_layer, cout, stride, relu;
+} sscater_upsampler;
+
 /* One stride's pillars (the full occupied set of the window).
  *   idx   : device int32[count], cell indices r*W + c, unique within the call;
  *           NULL with count == H*W selects dense mode: feats is then the whole
@@ -108,8 +120,12 @@ typedef struct {
     int64_t pairs[SSCATER_MAX_LAYERS + 1];  /* (input cell, output cell) pairs of layer l = 1..L */
     int64_t active_total[SSCATER_MAX_LAYERS + 1]; /* sums over all strides since create/reset */
     int64_t pairs_total[SSCATER_MAX_LAYERS + 1];
-    double flops;                           /* algorithmic flops of the last stride: sum_l 2*cin*cout*pairs_l */
+    double flops;                           /* algorithmic flops of the last stride: sum over layers and
+                                               upsamplers of 2*cin*cout*pairs */
     double bytes;                           /* algorithmic HBM bytes of the last stride */
+    int32_t n_ups;                          /* upsamplers of the neck */
+    int64_t up_pairs[SSCATER_MAX_UPSAMPLERS]; /* (input cell, output cell) pairs of upsampler u in the last
+                                                 stride: stride^2 per changed source cell */
 } sscater_stats_t;
 
 typedef struct sscater* sscater_t;
@@ -125,6 +141,18 @@ typedef struct sscater* sscater_t;
 int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
                    const void* const* weights, sscater_t* out);
 
+/* sscater_create with a neck: n_ups (0..SSCATER_MAX_UPSAMPLERS) upsamplers
+ * ups[u] with host weights up_weights[u] laid out [cin][cout][s][s] (the
+ * PyTorch ConvTranspose2d layout) in the grid dtype, copied and repacked.  The
+ * neck map is layer n_layers + 1 for sscater_read and sscater_changed; its
+ * change set is the union of the upsampled change sets of the source layers.
+ * Errors as sscater_create, plus SSCATER_E_INVALID_ARG for a source layer out
+ * of range, an unsupported (cin, cout, stride) or upsamplers that do not share
+ * one output grid. */
+int sscater_create_neck(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
+                        const void* const* weights, const sscater_upsampler* ups, int32_t n_ups,
+                        const void* const* up_weights, sscater_t* out);
+
 /* Advance by one stride (Alg. 1): detect the changed input cells, then for
  * each layer scatter the deltas into the persistent maps (Eq. 2) and build the
  * next layer's change list.  The first step after create/reset is the full
@@ -133,9 +161,10 @@ int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_
 int sscater_step(sscater_t h, const sscater_pillars* pillars, void* stream);
 
 /* Write layer `layer`'s output map into dst (device, NHWC, grid dtype):
- * layer 0 = the input canvas, layer l >= 1 = phi(Z_l) (bf16-rounded for the
- * bf16 dtype).  dst_bytes must be at least H_l*W_l*C_l*sizeof(dtype).
- * Asynchronous on `stream`. */
+ * layer 0 = the input canvas, layer l = 1..L = phi(Z_l) (bf16-rounded for the
+ * bf16 dtype), layer L + 1 = the neck map (each upsampler's phi over its
+ * channels) when the handle has a neck.  dst_bytes must be at least
+ * H_l*W_l*C_l*sizeof(dtype).  Asynchronous on `stream`. */
 int sscater_read(sscater_t h, int32_t layer, void* dst, size_t dst_bytes, void* stream);
 
 /* Return to the empty window: zero the canvas and maps, forget the change
@@ -147,7 +176,8 @@ int sscater_reset(sscater_t h, void* stream);
 int sscater_destroy(sscater_t h);
 
 /* Test / metrics extension: the last stride's change list A_layer
- * (0 <= layer <= L) sorted row-major into the HOST buffer dst[cap]; the list
+ * (0 <= layer <= L, or L + 1 for the neck) sorted row-major into the HOST
+ * buffer dst[cap]; the list
  * length goes to *count_host (also when it exceeds cap, in which case only cap
  * entries are written).  Synchronises `stream`. */
 int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32_t* count_host,
@@ -160,13 +190,14 @@ int sscater_stats(sscater_t h, sscater_stats_t* out, void* stream);
 /* Metrics extension: per-kernel timing with HIP events recorded on the
  * step's stream around every launch of sscater_step while enabled.  Slots:
  * 0 = input change detection (present pillars), 1 = vanished pillars,
- * 1 + l = layer l (l = 1..L), so L + 2 slots in all.  The events add a small
+ * 1 + l = layer l (l = 1..L), L + 2 + u = upsampler u of the neck, so
+ * L + 2 + n_ups slots in all.  The events add a small
  * gap between launches; enable it only for runs that measure kernels. */
 int sscater_profile(sscater_t h, int32_t enable);
 
 /* Sum of the timed launch durations per slot (milliseconds) and the number of
- * launches per slot since the previous read, into host arrays of n >= L + 2
- * entries; clears the record.  Synchronises `stream`. */
+ * launches per slot since the previous read, into host arrays of
+ * n >= L + 2 + n_ups entries; clears the record.  Synchronises `stream`. */
 int sscater_profile_read(sscater_t h, double* ms, int64_t* launches, int32_t n, void* stream);
 
 /* Static text for an error code; for SSCATER_E_HIP the last HIP error text of

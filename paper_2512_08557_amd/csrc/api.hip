@@ -43,6 +43,15 @@ struct LayerState {
     void* delta = nullptr;   // deltas of this layer's output, dense by cell (nullptr for the last layer)
 };
 
+// One upsampler of the neck.
+struct UpState {
+    sscater_upsampler spec{};
+    int cin = 0;
+    int Hs = 0, Ws = 0;      // source grid
+    int coff = 0;            // first channel in the neck map
+    void* wpack = nullptr;
+};
+
 thread_local char g_hip_err[256] = "no HIP error";
 
 int hip_fail(hipError_t e) {
@@ -63,6 +72,12 @@ struct sscater {
     bool bf16 = false;
     int row_bytes = 0;      // bytes of one input feature row
     LayerState layers[SSCATER_MAX_LAYERS];
+    // neck: upsamplers into one concatenated map on the grid Hn x Wn
+    int n_ups = 0;
+    UpState ups[SSCATER_MAX_UPSAMPLERS];
+    int Hn = 0, Wn = 0, Cn = 0;
+    float* Zn = nullptr;
+    uint32_t* stamp_n = nullptr;
     void* X = nullptr;
     uint64_t* pres = nullptr;
     uint32_t* stamp0 = nullptr;
@@ -198,8 +213,15 @@ const char* sscater_strerror(int code) {
 
 int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
                    const void* const* weights, sscater_t* out) {
+    return sscater_create_neck(grid, layers, n_layers, weights, nullptr, 0, nullptr, out);
+}
+
+int sscater_create_neck(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
+                        const void* const* weights, const sscater_upsampler* ups, int32_t n_ups,
+                        const void* const* up_weights, sscater_t* out) {
     // ---- validation: host only, before any HIP call ----
     if (!grid || !layers || !weights || !out) return SSCATER_E_INVALID_ARG;
+    if (n_ups < 0 || n_ups > SSCATER_MAX_UPSAMPLERS || (n_ups > 0 && (!ups || !up_weights))) return SSCATER_E_INVALID_ARG;
     *out = nullptr;
     if (grid->H <= 0 || grid->W <= 0 || grid->C0 <= 0 || grid->max_pillars < 0) return SSCATER_E_INVALID_ARG;
     if (grid->H >= 32768 || grid->W >= 32768) return SSCATER_E_INVALID_ARG;   // cell coordinates fit 15 bits
@@ -221,6 +243,27 @@ int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_
             H = out_extent(H, s.stride);
             W = out_extent(W, s.stride);
             C = s.cout;
+        }
+    }
+    // upsamplers: a backbone layer's output, kernel = stride in {1, 2, 4}, all
+    // onto one grid, concatenated
+    int Hn = 0, Wn = 0;
+    for (int u = 0; u < n_ups; ++u) {
+        const sscater_upsampler& up = ups[u];
+        if (up.src_layer < 1 || up.src_layer > n_layers || (up.relu != 0 && up.relu != 1) || !up_weights[u])
+            return SSCATER_E_INVALID_ARG;
+        int H = grid->H, W = grid->W;
+        for (int l = 0; l < up.src_layer; ++l) {
+            H = out_extent(H, layers[l].stride);
+            W = out_extent(W, layers[l].stride);
+        }
+        const int cin = layers[up.src_layer - 1].cout;
+        if (!upsample_supported(cin, up.cout, up.stride)) return SSCATER_E_INVALID_ARG;
+        if (u == 0) {
+            Hn = H * up.stride;
+            Wn = W * up.stride;
+        } else if (H * up.stride != Hn || W * up.stride != Wn) {
+            return SSCATER_E_INVALID_ARG;
         }
     }
 
@@ -270,7 +313,9 @@ int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_
             SSC_TRY(dev_alloc(h, (void**)&ls.Z, oc * ls.spec.cout * 4));
             SSC_TRY(dev_alloc(h, (void**)&ls.stamp, oc * 4));
             SSC_TRY(dev_alloc(h, (void**)&ls.list, oc * 4 * NSHARD));
-            if (l + 1 < n_layers) SSC_TRY(dev_alloc(h, &ls.delta, oc * ls.spec.cout * 4));
+            bool feeds_up = false;
+            for (int u = 0; u < n_ups; ++u) feeds_up = feeds_up || ups[u].src_layer == l + 1;
+            if (l + 1 < n_layers || feeds_up) SSC_TRY(dev_alloc(h, &ls.delta, oc * ls.spec.cout * 4));
             const size_t wn = wpack_elems(ls.spec.cin, ls.spec.cout, bf16);
             std::vector<unsigned char> packed(wn * esz);
             pack_weights(weights[l], ls.spec.cin, ls.spec.cout, bf16, packed.data());
@@ -280,6 +325,29 @@ int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_
             H = ls.Hout;
             W = ls.Wout;
         }
+    }
+    if (n_ups > 0) {
+        h->n_ups = n_ups;
+        h->Hn = Hn;
+        h->Wn = Wn;
+        for (int u = 0; u < n_ups; ++u) {
+            UpState& us = h->ups[u];
+            us.spec = ups[u];
+            const LayerState& src = h->layers[ups[u].src_layer - 1];
+            us.cin = src.spec.cout;
+            us.Hs = src.Hout;
+            us.Ws = src.Wout;
+            us.coff = h->Cn;
+            h->Cn += ups[u].cout;
+            const size_t wn = up_wpack_elems(us.cin, ups[u].cout, ups[u].stride, bf16);
+            std::vector<unsigned char> packed(wn * esz);
+            pack_up_weights(up_weights[u], us.cin, ups[u].cout, ups[u].stride, bf16, packed.data());
+            SSC_TRY(dev_alloc(h, &us.wpack, wn * esz));
+            he = hipMemcpy(us.wpack, packed.data(), wn * esz, hipMemcpyHostToDevice);
+            if (he != hipSuccess) { rc = hip_fail(he); goto fail; }
+        }
+        SSC_TRY(dev_alloc(h, (void**)&h->Zn, (size_t)Hn * Wn * h->Cn * 4));
+        SSC_TRY(dev_alloc(h, (void**)&h->stamp_n, (size_t)Hn * Wn * 4));
     }
     he = hipHostMalloc((void**)&h->err_host, 256, hipHostMallocMapped | hipHostMallocCoherent);
     if (he != hipSuccess) { h->err_host = nullptr; rc = hip_fail(he); goto fail; }
@@ -366,7 +434,7 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
         a.delta_in = l == 1 ? h->delta0 : h->layers[l - 2].delta;
         a.wpack = ls.wpack;
         a.Z = ls.Z;
-        a.delta_out = l < h->L ? ls.delta : nullptr;
+        a.delta_out = ls.delta;   // allocated when a later layer or an upsampler reads it
         a.Hin = ls.Hin;
         a.Win = ls.Win;
         a.Hout = ls.Hout;
@@ -382,6 +450,28 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
         }
         e = timed_launch(h, 1 + l, s, [&] {
             return launch_layer(a, ls.spec.cin, ls.spec.cout, ls.spec.stride, h->bf16, h->layer_grid, s);
+        });
+        if (e != hipSuccess) return hip_fail(e);
+    }
+
+    // the neck: every upsampler over its source layer's change list
+    for (int u = 0; u < h->n_ups; ++u) {
+        const UpState& us = h->ups[u];
+        const LayerState& src = h->layers[us.spec.src_layer - 1];
+        UpArgs a{};
+        a.list = src.list;
+        a.count = h->cnt_ptr(set, us.spec.src_layer);
+        a.cap = src.Hout * src.Wout;
+        a.delta_src = src.delta;
+        a.wpack = us.wpack;
+        a.Z = h->Zn;
+        a.ctot = h->Cn;
+        a.coff = us.coff;
+        a.stamp = h->stamp_n;
+        a.Wsrc = us.Ws;
+        a.epoch = epoch;
+        e = timed_launch(h, h->L + 2 + u, s, [&] {
+            return launch_upsample(a, us.cin, us.spec.cout, us.spec.stride, h->bf16, h->layer_grid, s);
         });
         if (e != hipSuccess) return hip_fail(e);
     }
@@ -402,7 +492,7 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
 }
 
 int sscater_read(sscater_t h, int32_t layer, void* dst, size_t dst_bytes, void* stream) {
-    if (!h || !dst || layer < 0 || layer > h->L) return SSCATER_E_INVALID_ARG;
+    if (!h || !dst || layer < 0 || layer > h->L + (h->n_ups > 0 ? 1 : 0)) return SSCATER_E_INVALID_ARG;
     if (int rc = check_sticky(h)) return rc;
     DeviceGuard dg(h->device);
     if (!dg.ok) return hip_fail(hipGetLastError());
@@ -413,6 +503,16 @@ int sscater_read(sscater_t h, int32_t layer, void* dst, size_t dst_bytes, void* 
         if (dst_bytes < need) return SSCATER_E_INVALID_ARG;
         hipError_t e = hipMemcpyAsync(dst, h->X, need, hipMemcpyDeviceToDevice, s);
         return e == hipSuccess ? SSCATER_OK : hip_fail(e);
+    }
+    if (layer == h->L + 1) {   // the neck map, each upsampler's phi over its channels
+        const long long cells = (long long)h->Hn * h->Wn;
+        if (dst_bytes < (size_t)cells * h->Cn * esz) return SSCATER_E_INVALID_ARG;
+        for (int u = 0; u < h->n_ups; ++u) {
+            const UpState& us = h->ups[u];
+            hipError_t e = launch_read_slice(h->Zn, dst, cells, h->Cn, us.coff, us.spec.cout, us.spec.relu, h->bf16, s);
+            if (e != hipSuccess) return hip_fail(e);
+        }
+        return SSCATER_OK;
     }
     const LayerState& ls = h->layers[layer - 1];
     const long long n = (long long)ls.Hout * ls.Wout * ls.spec.cout;
@@ -436,6 +536,7 @@ int sscater_reset(sscater_t h, void* stream) {
         const LayerState& ls = h->layers[l];
         e = launch_fill_zero(ls.Z, round_up((size_t)ls.Hout * ls.Wout * ls.spec.cout * 4, 256), s);
     }
+    if (e == hipSuccess && h->Zn) e = launch_fill_zero(h->Zn, round_up((size_t)h->Hn * h->Wn * h->Cn * 4, 256), s);
     if (e == hipSuccess) e = launch_fill_zero(h->counters, round_up((size_t)2 * h->ncnt() * 4, 256), s);
     if (e == hipSuccess) e = launch_fill_zero(h->cum, round_up((size_t)h->ncnt() * 8, 256), s);
     if (e != hipSuccess) return hip_fail(e);
@@ -460,7 +561,7 @@ int sscater_destroy(sscater_t h) {
 }
 
 int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32_t* count_host, void* stream) {
-    if (!h || !count_host || layer < 0 || layer > h->L || cap < 0 || (cap > 0 && !dst))
+    if (!h || !count_host || layer < 0 || layer > h->L + (h->n_ups > 0 ? 1 : 0) || cap < 0 || (cap > 0 && !dst))
         return SSCATER_E_INVALID_ARG;
     DeviceGuard dg(h->device);
     if (!dg.ok) return hip_fail(hipGetLastError());
@@ -472,19 +573,19 @@ int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32
         *count_host = 0;
         return SSCATER_OK;
     }
-    int32_t cnt[NSHARD * CSTRIDE];
-    e = hipMemcpy(cnt, h->cnt_ptr(h->last_set, layer), sizeof cnt, hipMemcpyDeviceToHost);
-    if (e != hipSuccess) return hip_fail(e);
     std::vector<int32_t> buf;
-    if (layer == 0) {
-        // A_0 is the set of input cells stamped with the last stride's epoch
-        const int cells = h->grid.H * h->grid.W;
+    if (layer == 0 || layer == h->L + 1) {
+        // A_0 and the neck's set: the cells stamped with the last stride's epoch
+        const int cells = layer == 0 ? h->grid.H * h->grid.W : h->Hn * h->Wn;
         std::vector<uint32_t> st((size_t)cells);
-        e = hipMemcpy(st.data(), h->stamp0, st.size() * 4, hipMemcpyDeviceToHost);
+        e = hipMemcpy(st.data(), layer == 0 ? h->stamp0 : h->stamp_n, st.size() * 4, hipMemcpyDeviceToHost);
         if (e != hipSuccess) return hip_fail(e);
         for (int q = 0; q < cells; ++q)
             if (st[(size_t)q] == h->last_epoch) buf.push_back(q);
     } else {
+        int32_t cnt[NSHARD * CSTRIDE];
+        e = hipMemcpy(cnt, h->cnt_ptr(h->last_set, layer), sizeof cnt, hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(e);
         // the list segments; a segment never holds more entries than its grid has cells
         const LayerState& ls = h->layers[layer - 1];
         const int cap_cells = ls.Hout * ls.Wout;
@@ -559,6 +660,18 @@ int sscater_stats(sscater_t h, sscater_stats_t* out, void* stream) {
                  + 9.0 * sp.cin * sp.cout * e_in     // weights
                  + 8.0 * (a_in + a_out);             // lists and stamps
     }
+    out->n_ups = h->n_ups;
+    for (int u = 0; u < h->n_ups; ++u) {
+        const UpState& us = h->ups[u];
+        const long long s2 = (long long)us.spec.stride * us.spec.stride;
+        const double a_src = (double)act[us.spec.src_layer];
+        out->up_pairs[u] = act[us.spec.src_layer] * s2;
+        flops += 2.0 * us.cin * us.spec.cout * a_src * (double)s2;
+        bytes += a_src * us.cin * e_d                              // source deltas
+                 + a_src * (double)s2 * us.spec.cout * 8.0         // neck Z read + write
+                 + (double)us.cin * us.spec.cout * s2 * e_in       // weights
+                 + a_src * (4.0 + (double)s2 * 4.0);               // list entries, stamps
+    }
     out->flops = flops;
     out->bytes = bytes;
     return check_sticky(h);
@@ -571,7 +684,7 @@ int sscater_profile(sscater_t h, int32_t enable) {
 }
 
 int sscater_profile_read(sscater_t h, double* ms, int64_t* launches, int32_t n, void* stream) {
-    if (!h || !ms || !launches || n < h->L + 2) return SSCATER_E_INVALID_ARG;
+    if (!h || !ms || !launches || n < h->L + 2 + h->n_ups) return SSCATER_E_INVALID_ARG;
     DeviceGuard dg(h->device);
     if (!dg.ok) return hip_fail(hipGetLastError());
     hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));

@@ -77,6 +77,21 @@ struct LayerArgs {
     int n_cum;
 };
 
+// One upsampler of the neck: transposed convolution (kernel = stride) of a
+// backbone layer's output deltas into the persistent concatenated neck map.
+struct UpArgs {
+    const int32_t* list;        // the source layer's change list: NSHARD segments of `cap` cells
+    const int32_t* count;       // segment lengths, segment k at count[k * CSTRIDE]
+    int cap;                    // cells of the source grid
+    const void* delta_src;      // source deltas, dense by cell [Hsrc*Wsrc][4*cin bytes]
+    const void* wpack;          // weights repacked for the MFMA operand layout
+    float* Z;                   // neck pre-activation map [Hn*Wn][ctot]
+    int ctot, coff;             // channels of the neck map, first channel of this upsampler
+    uint32_t* stamp;            // change stamps of the neck grid [Hn*Wn]
+    int Wsrc;                   // width of the source grid (Wn = stride * Wsrc)
+    uint32_t epoch;
+};
+
 enum ErrBits { ERR_INDEX_RANGE = 1, ERR_DUPLICATE = 2 };
 
 // Host-side launchers (defined in the kernel translation units).
@@ -86,6 +101,16 @@ bool layer_supported(int cin, int cout, int stride, bool bf16);
 hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, int grid,
                         hipStream_t s);
 hipError_t launch_read(const float* Z, void* dst, long long n, int relu, bool bf16, hipStream_t s);
+// phi of channels [coff, coff + cout) of a [cells][ctot] map into the same
+// channels of a [cells][ctot] destination.
+hipError_t launch_read_slice(const float* Z, void* dst, long long cells, int ctot, int coff, int cout, int relu,
+                             bool bf16, hipStream_t s);
+bool upsample_supported(int cin, int cout, int stride);
+hipError_t launch_upsample(const UpArgs& a, int cin, int cout, int stride, bool bf16, int grid, hipStream_t s);
+size_t up_wpack_elems(int cin, int cout, int stride, bool bf16);
+// Repack [cin][cout][S][S] transposed-conv weights (fp32 values, or bf16 bits)
+// into the layout the upsampling kernel reads.
+void pack_up_weights(const void* w, int cin, int cout, int stride, bool bf16, void* dst);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 size_t wpack_elems(int cin, int cout, bool bf16);
 // Repack OIHW weights (fp32 values, or bf16 bit patterns) into the layout the

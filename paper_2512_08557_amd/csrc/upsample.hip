@@ -1,0 +1,203 @@
+// Upsampling neck: transposed convolution with kernel = stride S on a backbone
+// block's output, on the changed cells only, into the persistent concatenated
+// neck map (Sec. III-B, backbone paragraph: the blocks are upsampled and
+// concatenated; Alg. 1, deconvolution branch: every upsampled site under a
+// changed site is changed).
+//
+// Kernel = stride, so output cell (S*i + a, S*j + b) has exactly one input
+// cell (i, j):  Z[S*i + a][S*j + b][co] += sum_ci dY[i][j][ci] * W[ci][co][a][b].
+// The delta form of Eq. 2 for this operator touches only the S x S block of
+// each changed input cell, each output cell is written by one workgroup, and
+// no atomics are needed.  The work list is the source layer's change list.
+//
+// Per changed input cell the contraction is [cin] x [cin x S*S*cout]: output
+// block ob = (a*S + b)*NCBT + cb holds 16 output channels of one sub-cell.
+// A workgroup takes a tile of 16 input cells and 4*BPW output blocks (4
+// wavefronts, BPW blocks each).  The tile's delta rows (the B operand of every
+// block) are copied once into LDS with asynchronous global->LDS copies shared
+// by the four wavefronts; each wavefront streams the weights of its blocks.
+#include "device_common.h"
+
+#include <algorithm>
+
+namespace ssc {
+
+template <int CIN, int COUT, int S, bool BF16>
+struct UpShape {
+    static constexpr int KTOT = BF16 ? 2 * CIN : CIN;
+    static constexpr int NCH = KTOT / (BF16 ? 32 : 16);   // 1 KB operand chunks
+    static constexpr int NCBT = COUT / 16;
+    static constexpr int NOB = S * S * NCBT;              // output blocks per input cell
+    static constexpr int BPW = NOB >= 8 ? 2 : 1;          // output blocks per wavefront
+    static constexpr int OBG = (NOB + 4 * BPW - 1) / (4 * BPW);   // workgroups per tile
+};
+
+template <int CIN, int COUT, int S, bool BF16>
+__global__ __launch_bounds__(256) void upsample_kernel(UpArgs a) {
+    using U = UpShape<CIN, COUT, S, BF16>;
+    constexpr int NCH = U::NCH, NOB = U::NOB, NCBT = U::NCBT, BPW = U::BPW, OBG = U::OBG;
+    constexpr int ROWB = 4 * CIN;                          // delta row bytes (fp32, or bf16 pair)
+    __shared__ uint4 As[NCH][64];
+
+    const int lane = (int)(threadIdx.x & 63u), wave = (int)(threadIdx.x >> 6);
+    const int cl = lane & 15, g = lane >> 4;
+    const int b = (int)blockIdx.x;
+    const int og = b % OBG;
+    const int shard = (b / OBG) % NSHARD;
+    const int TG = (int)gridDim.x / (OBG * NSHARD);        // workgroups per (segment, block group)
+    const int32_t* seg = a.list + (size_t)shard * a.cap;
+    const int n = a.count[shard * CSTRIDE];
+    const char* dbase = static_cast<const char*>(a.delta_src) + g * 16;
+    const uint4* wbase = static_cast<const uint4*>(a.wpack) + lane;
+    const int Wn = S * a.Wsrc;
+
+    int ob[BPW];
+    bool obv[BPW];
+#pragma unroll
+    for (int k = 0; k < BPW; ++k) {
+        const int o = (og * 4 + wave) * BPW + k;
+        obv[k] = o < NOB;
+        ob[k] = obv[k] ? o : 0;
+    }
+
+    for (int tile = (b / OBG) / NSHARD; tile * 16 < n; tile += TG) {
+        const int e = tile * 16 + cl;
+        const bool vrow = e < n;
+        const int p = vrow ? seg[min(e, a.cap - 1)] : 0;
+        const int i = p / a.Wsrc, j = p - (p / a.Wsrc) * a.Wsrc;
+        // the tile's delta rows: chunk c copied by wavefront c % 4
+#pragma unroll
+        for (int c = wave; c < NCH; c += 4)
+            __builtin_amdgcn_global_load_lds(
+                (const __attribute__((address_space(1))) void*)(dbase + (size_t)p * ROWB + c * 64),
+                (__attribute__((address_space(3))) void*)&As[c][0], 16, 0, 0);
+        // this wavefront's weights and old Z values, in the same round trip
+        uint4 bw[BPW][NCH];
+        f4v zo[BPW];
+        int oc[BPW];
+#pragma unroll
+        for (int k = 0; k < BPW; ++k) {
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) bw[k][c] = wbase[((size_t)c * NOB + ob[k]) * 64];
+            const int ab = ob[k] / NCBT, cb = ob[k] - (ob[k] / NCBT) * NCBT;
+            oc[k] = (S * i + ab / S) * Wn + (S * j + ab % S);
+            zo[k] = *reinterpret_cast<const f4v*>(a.Z + (size_t)oc[k] * a.ctot + a.coff + cb * 16 + 4 * g);
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();                                   // every chunk of the tile has landed
+
+        f4v acc[BPW];
+#pragma unroll
+        for (int k = 0; k < BPW; ++k) acc[k] = f4v{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const uint4 av = As[c][lane];
+#pragma unroll
+            for (int k = 0; k < BPW; ++k) {
+                if constexpr (BF16) {
+                    bf8v A, B;
+                    __builtin_memcpy(&A, &bw[k][c], 16);
+                    __builtin_memcpy(&B, &av, 16);
+                    acc[k] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B, acc[k], 0, 0, 0);
+                } else {
+                    acc[k] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bw[k][c].x), __uint_as_float(av.x), acc[k], 0, 0, 0);
+                    acc[k] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bw[k][c].y), __uint_as_float(av.y), acc[k], 0, 0, 0);
+                    acc[k] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bw[k][c].z), __uint_as_float(av.z), acc[k], 0, 0, 0);
+                    acc[k] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(bw[k][c].w), __uint_as_float(av.w), acc[k], 0, 0, 0);
+                }
+            }
+        }
+        if (vrow) {
+#pragma unroll
+            for (int k = 0; k < BPW; ++k) {
+                if (!obv[k]) continue;
+                const int cb = ob[k] - (ob[k] / NCBT) * NCBT;
+                f4v zn;
+                zn.x = zo[k].x + acc[k].x;
+                zn.y = zo[k].y + acc[k].y;
+                zn.z = zo[k].z + acc[k].z;
+                zn.w = zo[k].w + acc[k].w;
+                *reinterpret_cast<f4v*>(a.Z + (size_t)oc[k] * a.ctot + a.coff + cb * 16 + 4 * g) = zn;
+                if (g == 0) a.stamp[oc[k]] = a.epoch;      // every writer stores the same value
+            }
+        }
+        __syncthreads();                                   // the chunks are consumed
+    }
+}
+
+#define SSC_UP_SHAPES(X)                                                                                    \
+    X(64, 128, 1) X(64, 64, 1) X(64, 32, 1) X(64, 16, 1) X(128, 128, 2) X(128, 64, 2) X(128, 128, 1)        \
+    X(256, 128, 4) X(256, 64, 4) X(256, 128, 2) X(32, 32, 1) X(32, 32, 2) X(16, 16, 1) X(16, 16, 2)          \
+    X(16, 32, 2) X(16, 16, 4) X(32, 16, 4) X(64, 32, 2) X(64, 64, 2) X(64, 64, 4)
+
+bool upsample_supported(int cin, int cout, int stride) {
+#define SSC_SUP(CI, CO, S) if (cin == CI && cout == CO && stride == S) return true;
+    SSC_UP_SHAPES(SSC_SUP)
+#undef SSC_SUP
+    return false;
+}
+
+template <int CI, int CO, int S, bool BF16>
+static hipError_t launch_up_shape(const UpArgs& a, int grid, hipStream_t s) {
+    using U = UpShape<CI, CO, S, BF16>;
+    // tile slots per (segment, block group); at most ceil(cap / 16) tiles per segment
+    int tg = std::max(1, grid / (U::OBG * NSHARD));
+    tg = std::min(tg, std::max(1, (a.cap + 15) / 16));
+    hipLaunchKernelGGL((upsample_kernel<CI, CO, S, BF16>), dim3(tg * U::OBG * NSHARD), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_upsample(const UpArgs& a, int cin, int cout, int stride, bool bf16, int grid, hipStream_t s) {
+#define SSC_LAUNCH(CI, CO, S)                                                                               \
+    if (cin == CI && cout == CO && stride == S)                                                             \
+        return bf16 ? launch_up_shape<CI, CO, S, true>(a, grid, s) : launch_up_shape<CI, CO, S, false>(a, grid, s);
+    SSC_UP_SHAPES(SSC_LAUNCH)
+#undef SSC_LAUNCH
+    return hipErrorInvalidValue;
+}
+
+size_t up_wpack_elems(int cin, int cout, int stride, bool bf16) {
+    return (size_t)(bf16 ? 2 * cin : cin) * (size_t)cout * stride * stride;
+}
+
+// Layout, in 16-byte lane vectors: [chunk c][output block ob][lane l], with
+// ob = (a*S + b)*NCBT + cb; lane l of block ob holds output channel
+// cb*16 + l%16 of sub-cell (a, b) and the k-group l/16 of chunk c: fp32
+// k = c*16 + 4*(l/16) + e (e < 4); bf16 k = c*32 + 8*(l/16) + e (e < 8) over
+// the pair [W | -W].  w: [cin][cout][S][S] (fp32 values, or bf16 bits).
+void pack_up_weights(const void* w, int cin, int cout, int s, bool bf16, void* dst) {
+    const int ncbt = cout / 16, nob = s * s * ncbt;
+    auto widx = [&](int ci, int co, int a, int b) { return (((size_t)ci * cout + co) * s + a) * s + b; };
+    if (!bf16) {
+        const float* src = static_cast<const float*>(w);
+        float* out = static_cast<float*>(dst);
+        const int nch = cin / 16;
+        for (int c = 0; c < nch; ++c)
+            for (int ob = 0; ob < nob; ++ob) {
+                const int ab = ob / ncbt, cb = ob % ncbt;
+                for (int l = 0; l < 64; ++l)
+                    for (int e = 0; e < 4; ++e) {
+                        const int co = cb * 16 + l % 16, ci = c * 16 + 4 * (l / 16) + e;
+                        out[(((size_t)c * nob + ob) * 64 + l) * 4 + e] = src[widx(ci, co, ab / s, ab % s)];
+                    }
+            }
+    } else {
+        const uint16_t* src = static_cast<const uint16_t*>(w);
+        uint16_t* out = static_cast<uint16_t*>(dst);
+        const int nch = (2 * cin) / 32;
+        for (int c = 0; c < nch; ++c)
+            for (int ob = 0; ob < nob; ++ob) {
+                const int ab = ob / ncbt, cb = ob % ncbt;
+                for (int l = 0; l < 64; ++l)
+                    for (int e = 0; e < 8; ++e) {
+                        const int co = cb * 16 + l % 16, k = c * 32 + 8 * (l / 16) + e;
+                        const int ci = k < cin ? k : k - cin;
+                        uint16_t v = src[widx(ci, co, ab / s, ab % s)];
+                        if (k >= cin) v ^= 0x8000u;   // -W: exact sign flip
+                        out[(((size_t)c * nob + ob) * 64 + l) * 8 + e] = v;
+                    }
+            }
+    }
+}
+
+}  // namespace ssc

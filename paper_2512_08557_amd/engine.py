@@ -18,12 +18,14 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libsscater.so")
 
 MAX_LAYERS = 32
+MAX_UPSAMPLERS = 4
 OK, E_INVALID_ARG, E_OUT_OF_MEMORY, E_HIP, E_OVERFLOW, E_DEVICE = 0, -1, -2, -3, -4, -5
 F32, BF16 = 0, 1
 
 # every function declared in include/sscater.h
-EXPORTS = ("sscater_create", "sscater_step", "sscater_read", "sscater_reset", "sscater_destroy",
-           "sscater_changed", "sscater_stats", "sscater_profile", "sscater_profile_read", "sscater_strerror")
+EXPORTS = ("sscater_create", "sscater_create_neck", "sscater_step", "sscater_read", "sscater_reset",
+           "sscater_destroy", "sscater_changed", "sscater_stats", "sscater_profile", "sscater_profile_read",
+           "sscater_strerror")
 
 
 class Grid(ctypes.Structure):
@@ -36,6 +38,11 @@ class Layer(ctypes.Structure):
                 ("stride", ctypes.c_int32), ("pad", ctypes.c_int32), ("relu", ctypes.c_int32)]
 
 
+class Upsampler(ctypes.Structure):
+    _fields_ = [("src_layer", ctypes.c_int32), ("cout", ctypes.c_int32), ("stride", ctypes.c_int32),
+                ("relu", ctypes.c_int32)]
+
+
 class Pillars(ctypes.Structure):
     _fields_ = [("idx", ctypes.c_void_p), ("feats", ctypes.c_void_p), ("count", ctypes.c_int32)]
 
@@ -45,7 +52,8 @@ class Stats(ctypes.Structure):
                 ("active", ctypes.c_int64 * (MAX_LAYERS + 1)), ("pairs", ctypes.c_int64 * (MAX_LAYERS + 1)),
                 ("active_total", ctypes.c_int64 * (MAX_LAYERS + 1)),
                 ("pairs_total", ctypes.c_int64 * (MAX_LAYERS + 1)),
-                ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
+                ("flops", ctypes.c_double), ("bytes", ctypes.c_double), ("n_ups", ctypes.c_int32),
+                ("up_pairs", ctypes.c_int64 * MAX_UPSAMPLERS)]
 
 
 class SscaterError(RuntimeError):
@@ -66,6 +74,9 @@ def lib() -> ctypes.CDLL:
         vp, i32 = ctypes.c_void_p, ctypes.c_int32
         L.sscater_create.argtypes = [ctypes.POINTER(Grid), ctypes.POINTER(Layer), i32,
                                      ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(vp)]
+        L.sscater_create_neck.argtypes = [ctypes.POINTER(Grid), ctypes.POINTER(Layer), i32,
+                                          ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(Upsampler), i32,
+                                          ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(vp)]
         L.sscater_step.argtypes = [vp, ctypes.POINTER(Pillars), vp]
         L.sscater_read.argtypes = [vp, i32, vp, ctypes.c_size_t, vp]
         L.sscater_reset.argtypes = [vp, vp]
@@ -108,7 +119,11 @@ class Engine:
     """One handle of the delta-scatter backbone state (one sensor stream)."""
 
     def __init__(self, H: int, W: int, C0: int, layers: Sequence[Tuple[int, int, int, bool]],
-                 weights: Sequence[np.ndarray], dtype: str = "f32", max_pillars: int = 16000):
+                 weights: Sequence[np.ndarray], dtype: str = "f32", max_pillars: int = 16000,
+                 ups: Sequence[Tuple[int, int, int, bool]] = (), up_weights: Sequence[np.ndarray] = ()):
+        """layers: (cin, cout, stride, relu); weights: OIHW per layer.  ups:
+        optional neck, (src_layer, cout, stride, relu) per upsampler with
+        [cin, cout, s, s] weights; the neck map is layer len(layers) + 1."""
         import torch  # device memory and streams only
         self._torch = torch
         self.H, self.W, self.C0 = H, W, C0
@@ -127,7 +142,22 @@ class Engine:
             raise ValueError("one weight tensor per layer")
         wptrs = (ctypes.c_void_p * n)(*[b.ctypes.data for b in self._wbufs])
         handle = ctypes.c_void_p()
-        _check(lib().sscater_create(ctypes.byref(grid), larr, n, wptrs, ctypes.byref(handle)), "sscater_create")
+        self.ups = [tuple(u) for u in ups]
+        if self.ups:
+            nu = len(self.ups)
+            if len(up_weights) != nu:
+                raise ValueError("one weight tensor per upsampler")
+            self._ubufs = [weights_to_dtype_bytes(wt, dtype) for wt in up_weights]
+            uarr = (Upsampler * nu)(*[Upsampler(src, co, s, int(bool(r))) for (src, co, s, r) in self.ups])
+            uptrs = (ctypes.c_void_p * nu)(*[b.ctypes.data for b in self._ubufs])
+            _check(lib().sscater_create_neck(ctypes.byref(grid), larr, n, wptrs, uarr, nu, uptrs,
+                                             ctypes.byref(handle)), "sscater_create_neck")
+            src0, _co, s0, _r = self.ups[0]
+            hs, ws_, _c = self.shapes[src0]
+            self.shapes.append((hs * s0, ws_ * s0, sum(u[1] for u in self.ups)))
+            self._ubufs = None
+        else:
+            _check(lib().sscater_create(ctypes.byref(grid), larr, n, wptrs, ctypes.byref(handle)), "sscater_create")
         self._h = handle
         self._wbufs = None   # copied by the library
 
@@ -184,14 +214,16 @@ class Engine:
         L = st.n_layers
         return dict(steps=st.steps, pillars=st.pillars, active=list(st.active[:L + 1]),
                     pairs=list(st.pairs[:L + 1]), active_total=list(st.active_total[:L + 1]),
-                    pairs_total=list(st.pairs_total[:L + 1]), flops=st.flops, bytes=st.bytes)
+                    pairs_total=list(st.pairs_total[:L + 1]), flops=st.flops, bytes=st.bytes,
+                    up_pairs=list(st.up_pairs[:st.n_ups]))
 
     def profile(self, enable: bool) -> None:
         _check(lib().sscater_profile(self._h, int(bool(enable))), "sscater_profile")
 
     def profile_read(self, stream=None):
-        """(ms per slot, launches per slot); slot 0 detect, 1 vanished, 1+l layer l."""
-        n = len(self.layers) + 2
+        """(ms per slot, launches per slot); slot 0 detect, 1 vanished, 1+l layer l,
+        L+2+u upsampler u."""
+        n = len(self.layers) + 2 + len(self.ups)
         ms = (ctypes.c_double * n)()
         cnt = (ctypes.c_int64 * n)()
         _check(lib().sscater_profile_read(self._h, ms, cnt, n, self._stream(stream)), "sscater_profile_read")

@@ -104,3 +104,45 @@ def test_weight_marshalling_for_bf16():
     assert b.dtype == np.uint16 and b.tolist() == [0x3F80, 0xC020, 0x3E20]
     with pytest.raises(ValueError):
         E.weights_to_dtype_bytes(np.array([0.1], np.float32), "bf16")
+
+
+def _create_neck(grid, layers, ups, up_w=True):
+    lib = ssc.lib()
+    n = len(layers)
+    larr = (E.Layer * n)(*layers)
+    bufs = [np.zeros((l.cout, l.cin, 3, 3), np.float32) for l in layers]
+    wp = (ctypes.c_void_p * n)(*[b.ctypes.data for b in bufs])
+    nu = len(ups)
+    uarr = (E.Upsampler * max(nu, 1))(*ups)
+    cins = [layers[u.src_layer - 1].cout if 1 <= u.src_layer <= n else 16 for u in ups]
+    ubufs = [np.zeros((ci, u.cout, max(u.stride, 1), max(u.stride, 1)), np.float32) for ci, u in zip(cins, ups)]
+    up = (ctypes.c_void_p * max(nu, 1))(*[b.ctypes.data for b in ubufs]) if up_w else None
+    h = ctypes.c_void_p()
+    rc = lib.sscater_create_neck(ctypes.byref(grid), larr, n, wp, uarr, nu, up, ctypes.byref(h))
+    if rc == ssc.OK:
+        lib.sscater_destroy(h)
+    return rc
+
+
+@pytest.mark.parametrize("case", ["src0", "src_beyond", "stride3", "unsupported", "grid_mismatch", "null_weights",
+                                  "too_many"])
+def test_create_neck_rejects_invalid_arguments(case):
+    g = E.Grid(32, 32, 64, 100, E.F32)
+    L = [E.Layer(64, 64, 3, 2, 1, 1), E.Layer(64, 128, 3, 2, 1, 1)]     # 16x16x64, then 8x8x128
+    ups = [E.Upsampler(1, 128, 1, 1), E.Upsampler(2, 128, 2, 1)]        # both onto 16x16
+    up_w = True
+    if case == "src0":
+        ups[0].src_layer = 0
+    elif case == "src_beyond":
+        ups[1].src_layer = 3
+    elif case == "stride3":
+        ups[1].stride = 3
+    elif case == "unsupported":
+        ups[0].cout = 48
+    elif case == "grid_mismatch":
+        ups[1].stride = 4                                                 # 8x8 -> 32x32, not 16x16
+    elif case == "null_weights":
+        up_w = False
+    elif case == "too_many":
+        ups = ups * 3
+    assert _create_neck(g, L, ups, up_w) == ssc.E_INVALID_ARG
