@@ -68,21 +68,27 @@ def upload(strides, dtype):
     return out
 
 
-def kernel_name(slot: int, wl) -> str:
+def kernel_name(slot: int, wl, ups=()) -> str:
     if slot == 0:
         return "detect_kernel<present>"
     if slot == 1:
         return "detect_kernel<vanished>"
+    if slot >= len(wl.layers) + 2:
+        u = ups[slot - len(wl.layers) - 2]
+        cin = wl.layers[u.src - 1].cout
+        return f"upsample_kernel<{cin},{u.cout},{u.stride},{wl.dtype}>"
     l = wl.layers[slot - 2]
     return f"layer_kernel<{l.cin},{l.cout},{l.stride},{wl.dtype}>"
 
 
-def cpu_baseline(wl, ws, strides, first, budget_s):
-    """The oracle as it stands (dense float64 recompute of every layer plus the
-    change lists) on consecutive strides of the timed range, until the time
-    budget is spent."""
+def cpu_baseline(wl, ws, strides, first, budget_s, neck=()):
+    """The oracle as it stands (dense float64 recompute of every layer, and of
+    the neck when there is one, plus the change lists) on consecutive strides
+    of the timed range, until the time budget is spent."""
     import oracle
     layers = layers_of(wl)
+    ups = [(u.src, u.cout, u.stride, u.relu) for u in neck]
+    uw = S.neck_weights(wl.name) if neck else []
     prev = oracle.canvas_bits(S.canvas(strides[first - 1], wl.H, wl.W, wl.C0), wl.dtype)
     t_total, u_total, n = 0.0, 0, 0
     for st in strides[first:]:
@@ -90,17 +96,20 @@ def cpu_baseline(wl, ws, strides, first, budget_s):
         t0 = time.perf_counter()
         bits = oracle.canvas_bits(canvas, wl.dtype)
         x = oracle.exact_canvas(canvas, wl.dtype)
-        oracle.forward(x, ws, layers, bf16_storage=(wl.dtype == "bf16"))
+        ys = oracle.forward(x, ws, layers, bf16_storage=(wl.dtype == "bf16"))
         lists = oracle.changed_lists(prev, bits, [l[2] for l in layers])
+        if ups:
+            oracle.forward_neck(ys, uw, ups, bf16_storage=(wl.dtype == "bf16"))
         t_total += time.perf_counter() - t0
-        u_total += sum(len(a) for a in lists[:-1])
+        u_total += sum(len(a) for a in lists[:-1]) + sum(len(lists[u[0]]) for u in ups)
         prev = bits
         n += 1
         if t_total >= budget_s:
             break
     return {"value": u_total / t_total, "unit": "updates/s", "cores": oracle.threads(), "kind": "oracle",
             "sample": f"{n} consecutive delta strides of the timed range, each a dense float64 recompute of "
-                      f"all {len(layers)} layers plus the per-layer change lists ({t_total:.1f} s, "
+                      f"all {len(layers)} layers{' and the neck' if ups else ''} plus the per-layer change lists "
+                      f"({t_total:.1f} s, "
                       f"{t_total / n * 1e3:.1f} ms per stride)"}
 
 
@@ -257,6 +266,7 @@ def main() -> int:
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
     ap.add_argument("--no-full", action="store_true", help="skip the GPU full-recompute timing")
+    ap.add_argument("--neck", action="store_true", help="include the upsampling neck (c3, c4)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     ap.add_argument("--digest-trace", metavar="CSV", help="summarise a rocprofv3 kernel-trace csv and exit")
@@ -296,7 +306,12 @@ def main() -> int:
     log(f"[bench] workload {wl.name}: {wl.description}; generating {W + K} delta strides")
     strides = S.make_stream(wl.name, n_strides=W + K)
     dev = upload(strides, wl.dtype)
-    eng = Engine(wl.H, wl.W, wl.C0, layers_of(wl), ws, dtype=wl.dtype, max_pillars=wl.max_pillars)
+    neck = S.neck(wl.name) if args.neck else ()
+    if args.neck and not neck:
+        log(f"bench.py: workload {wl.name} has no neck")
+        return 2
+    eng = Engine(wl.H, wl.W, wl.C0, layers_of(wl), ws, dtype=wl.dtype, max_pillars=wl.max_pillars,
+                 ups=[(u.src, u.cout, u.stride, u.relu) for u in neck], up_weights=S.neck_weights(wl.name) if neck else ())
     L = len(wl.layers)
 
     def run_range(lo, hi):
@@ -332,6 +347,7 @@ def main() -> int:
     act_in = [after["active_total"][l] - before["active_total"][l] for l in range(L + 1)]
     pairs = [after["pairs_total"][l] - before["pairs_total"][l] for l in range(L + 1)]
     updates = sum(act_in[:L])          # sum_l |A_{l-1}| over the timed strides
+    updates += sum(act_in[u.src] for u in neck)   # each upsampler takes its source layer's changed cells
     ms_per_step = wall_ms / K
     value = updates / (wall_ms / 1e3)
     log(f"[bench] {K} strides in {wall_ms:.2f} ms -> {ms_per_step * 1e3:.1f} us/stride, "
@@ -353,14 +369,14 @@ def main() -> int:
         pairs2 = [a2["pairs_total"][l] - b2["pairs_total"][l] for l in range(L + 1)]
         act2 = [a2["active_total"][l] - b2["active_total"][l] for l in range(L + 1)]
         e_d = 4.0
-        for slot in range(L + 2):
+        for slot in range(L + 2 + len(neck)):
             if cnt[slot] == 0:
                 continue
-            name = kernel_name(slot, wl)
+            name = kernel_name(slot, wl, neck)
             k = kernels.setdefault(name, {"ms": 0.0, "launches": 0, "flops": 0.0, "bytes": 0.0})
             k["ms"] += ms[slot]
             k["launches"] += cnt[slot]
-            if slot >= 2:
+            if 2 <= slot < L + 2:
                 l = slot - 1
                 sp = wl.layers[l - 1]
                 k["flops"] += 2.0 * sp.cin * sp.cout * pairs2[l]
@@ -429,7 +445,7 @@ def main() -> int:
     if not args.no_cpu:
         try:
             log(f"[bench] CPU oracle baseline (budget {args.cpu_seconds:.0f} s)")
-            cpu = cpu_baseline(wl, ws, strides, 1 + W, args.cpu_seconds)
+            cpu = cpu_baseline(wl, ws, strides, 1 + W, args.cpu_seconds, neck)
         except Exception as exc:  # the oracle is optional for the GPU number
             log(f"[bench] CPU baseline skipped: {exc}")
 
@@ -440,6 +456,7 @@ def main() -> int:
         "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.description}", "grid": f"{wl.W}x{wl.H}", "C0": wl.C0,
                    "layers": [f"{l.cin}->{l.cout} s{l.stride}{' relu' if l.relu else ''}" for l in wl.layers],
+                   "neck": [f"up(layer {u.src}) {wl.layers[u.src - 1].cout}->{u.cout} x{u.stride}" for u in neck],
                    "strides": "full window + warmup untimed, then the timed delta strides",
                    "mean_pillars": float(np.mean([len(s.idx) for s in strides[1 + W:]])),
                    "mean_active": [a / K for a in act_in]},
