@@ -272,8 +272,8 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
 // deltas, so a workgroup covers 2 tiles x 2 output-channel blocks (4
 // wavefronts, one tile and one block each; the cout dimension is spread over
 // NCBT/2 workgroups) and streams both operands tap by tap through LDS with
-// asynchronous global->LDS copies, double-buffered: while the matrix cores
-// work on tap t from registers, the copies of the next tap are in flight.
+// asynchronous global->LDS copies: while the matrix cores work on tap t from
+// registers, the copies of the next tap are in flight.
 // Each copy is shared by the two wavefronts that need it (a vector load of the
 // same bytes by every wavefront costs several times more per compute unit).
 // Stage layout: [slot][chunk][lane] with slots tile 0, tile 1, block 0,
@@ -294,7 +294,7 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
     constexpr int NCH = W::NCH, NCBT = W::NCBT, NH = W::NH;
     constexpr int ROWB_IN = 4 * CIN;
     static_assert(NCH % 2 == 0 && NCBT % 2 == 0, "shape");
-    __shared__ uint4 stage[2][4][NCH][64];
+    __shared__ uint4 stage[4][NCH][64];
     __shared__ int tapmask;
 
     const int lane = (int)(threadIdx.x & 63u), wave = (int)(threadIdx.x >> 6);
@@ -335,45 +335,51 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
         __syncthreads();
         unsigned taps = (unsigned)tapmask;
 
-        // copies of tap t into buffer bi: the two wavefronts of a tile share
+        // copies of tap t into the stage: the two wavefronts of a tile share
         // its delta chunks, the two wavefronts of a cout block its weights
-        auto issue = [&](int t, int bi) __attribute__((always_inline)) {
+        auto issue = [&](int t) __attribute__((always_inline)) {
             const int row = max(rows[t], 0);
 #pragma unroll
             for (int c = cbl; c < NCH; c += 2)
                 __builtin_amdgcn_global_load_lds(
                     (const __attribute__((address_space(1))) void*)(dbase + (size_t)row * ROWB_IN + c * 64),
-                    (__attribute__((address_space(3))) void*)&stage[bi][tp][c][0], 16, 0, 0);
+                    (__attribute__((address_space(3))) void*)&stage[tp][c][0], 16, 0, 0);
 #pragma unroll
             for (int c = tp; c < NCH; c += 2)
                 __builtin_amdgcn_global_load_lds(
                     (const __attribute__((address_space(1))) void*)(wbase + ((size_t)(t * NCH + c) * NCBT + cbg) * 64),
-                    (__attribute__((address_space(3))) void*)&stage[bi][2 + cbl][c][0], 16, 0, 0);
+                    (__attribute__((address_space(3))) void*)&stage[2 + cbl][c][0], 16, 0, 0);
         };
 
+        // one stage buffer: a tap's operands move to registers, then the
+        // copies of the next tap overwrite the stage while the matrix cores
+        // work; a small stage lets two workgroups share a compute unit, so
+        // one computes while the other waits for its copies
         f4v acc[1] = {f4v{0.f, 0.f, 0.f, 0.f}};
-        int bi = 0;
-        if (taps) issue(__builtin_ctz(taps), 0);
+        if (taps) issue(__builtin_ctz(taps));
         while (taps) {
             const int t = __builtin_ctz(taps);
             taps &= taps - 1u;
             __builtin_amdgcn_s_waitcnt(0);             // this wavefront's copies of tap t
-            __syncthreads();                           // everyone's copies of tap t; buffer bi^1 is free
+            __syncthreads();                           // everyone's copies of tap t
             uint4 av[NCH], bv[NCH];
             const uint32_t m = rows[t] >= 0 ? ~0u : 0u;   // unchanged input: zero row
 #pragma unroll
             for (int c = 0; c < NCH; ++c) {
-                const uint4 x = stage[bi][tp][c][lane];
+                const uint4 x = stage[tp][c][lane];
                 av[c] = make_uint4(x.x & m, x.y & m, x.z & m, x.w & m);
-                bv[c] = stage[bi][2 + cbl][c][lane];
+                bv[c] = stage[2 + cbl][c][lane];
             }
-            if (taps) issue(__builtin_ctz(taps), bi ^ 1);
+            if (taps) {
+                __builtin_amdgcn_s_waitcnt(0);         // this wavefront's stage reads are done
+                __syncthreads();                       // everyone's: the stage is free
+                issue(__builtin_ctz(taps));
+            }
 #pragma unroll
             for (int c = 0; c < NCH; ++c) {
                 const uint4 bb[1] = {bv[c]};
                 mfma_chunk<BF16, 1>(acc, av[c], bb);
             }
-            bi ^= 1;
         }
         if (vrow) epilogue4<COUT, BF16>(a, q, cbg * 16 + 4 * g, zo, acc[0]);
         if (do_prop) prop_finish<4>(a.next, a.epoch, shard, pb);
