@@ -18,7 +18,8 @@ Printed: one JSON line with
                (one changed input cell pushed through one layer's 3x3 filter bank)
   ms_per_step  wall-clock ms per stride over the timed region
   roofline     the dominant kernel's algorithmic flops (or bytes) per launch over
-               its HIP-event-timed duration, against the MI355X peak
+               its duration from HIP events stamped by the kernel's dispatch,
+               against the MI355X peak
   cpu_baseline the CPU oracle (dense float64 recompute) on a bounded sample of the
                same strides
 """
@@ -180,7 +181,7 @@ def _csv_rows(path):
 def digest_trace(path: str, steps: int, warmup: int, wl) -> str:
     """Markdown tables of a --kernel-trace csv of the default bench command:
     three passes of (full window, warmup, the timed strides) -- timed, with an
-    event after every stride, with events around every launch -- then the
+    event after every stride, with events stamped by every launch -- then the
     full recomputes."""
     rows = sorted(_csv_rows(path), key=lambda r: int(r["Start_Timestamp"]))
     by = {}
@@ -201,7 +202,7 @@ def digest_trace(path: str, steps: int, warmup: int, wl) -> str:
         first = 0 if k.endswith("vanished>") else 1   # no vanish pass on a full window
         span = (first + warmup + steps) * n            # launches of one pass
         a0, a1 = (first + warmup) * n, (first + warmup + steps) * n
-        b0, b1 = 2 * span + a0, 2 * span + a1          # third pass: events around every launch
+        b0, b1 = 2 * span + a0, 2 * span + a1          # third pass: events stamped by every launch
         if len(v) >= b1:
             out.append(f"| {k} | {statistics.fmean(v[a0:a1]):.2f} | {statistics.fmean(v[b0:b1]):.2f} |")
     return "\n".join(out)
@@ -353,7 +354,7 @@ def main() -> int:
     log(f"[bench] {K} strides in {wall_ms:.2f} ms -> {ms_per_step * 1e3:.1f} us/stride, "
         f"{value:.3e} updates/s; mean |A_l| = {[round(a / K) for a in act_in]}")
 
-    # ---- per-kernel pass: same strides, HIP events around every launch ----
+    # ---- per-kernel pass: same strides, HIP events stamped by every launch ----
     roofline = None
     kernels = {}
     if not args.no_profile:
@@ -384,26 +385,12 @@ def main() -> int:
                                (act2[l] * sp.cout * e_d if l < L else 0.0) +
                                cnt[slot] * 9.0 * sp.cin * sp.cout * (2 if wl.dtype == "bf16" else 4) +
                                8.0 * (act2[l - 1] + act2[l]))
-        # an event pair with nothing between it, on the same stream: the part of
-        # an event-bracketed launch that is not the kernel itself
-        pair_ms = []
-        for _ in range(3):
-            evp = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(64)]
-            torch.cuda.synchronize()
-            for e0, e1 in evp:
-                e0.record(stream)
-                e1.record(stream)
-            torch.cuda.synchronize()
-            pair_ms.append(statistics.median(e0.elapsed_time(e1) for e0, e1 in evp))
-        pair_us = min(pair_ms) * 1e3
         for name, k in kernels.items():
             log(f"[bench] {name:34s} {k['launches']:5d} launches  avg {k['ms'] / k['launches'] * 1e3:8.2f} us  "
                 f"total {k['ms']:.3f} ms")
-        log(f"[bench] empty event pair on the stream: {pair_us:.2f} us")
         dom_name, dom = max(kernels.items(), key=lambda kv: kv[1]["ms"])
         if dom["flops"] > 0:
-            # the event-bracketed duration includes the dispatch of the kernel and
-            # the two timestamp packets (conservative: it only lowers `achieved`)
+            # start and end stamped by the kernel's own dispatch packet
             launch_us = dom["ms"] / dom["launches"] * 1e3
             secs = launch_us * 1e-6 * dom["launches"]
             intensity = dom["flops"] / max(dom["bytes"], 1.0)
@@ -419,7 +406,6 @@ def main() -> int:
                             "frac": achieved / PEAK_HBM_GBS, "traffic": traffic}
             roofline.update({"kernel": dom_name, "launches": dom["launches"],
                              "avg_launch_us": launch_us,
-                             "empty_event_pair_us": pair_us,
                              "alg_flops_per_launch": dom["flops"] / dom["launches"],
                              "alg_bytes_per_launch": dom["bytes"] / dom["launches"],
                              "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "

@@ -187,12 +187,13 @@ int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32
  * Synchronises `stream`. */
 int sscater_stats(sscater_t h, sscater_stats_t* out, void* stream);
 
-/* Metrics extension: per-kernel timing with HIP events recorded on the
- * step's stream around every launch of sscater_step while enabled.  Slots:
+/* Metrics extension: per-kernel timing of every launch of sscater_step while
+ * enabled, with a pair of HIP events that the kernel's own dispatch stamps at
+ * its start and end (hipExtLaunchKernel), so the figure is the kernel's
+ * execution time without the event packets' cost.  Slots:
  * 0 = input change detection (present pillars), 1 = vanished pillars,
  * 1 + l = layer l (l = 1..L), L + 2 + u = upsampler u of the neck, so
- * L + 2 + n_ups slots in all.  The events add a small
- * gap between launches; enable it only for runs that measure kernels. */
+ * L + 2 + n_ups slots in all.  Enable it only for runs that measure kernels. */
 int sscater_profile(sscater_t h, int32_t enable);
 
 /* Sum of the timed launch durations per slot (milliseconds) and the number of

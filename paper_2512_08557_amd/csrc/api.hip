@@ -164,18 +164,20 @@ hipError_t prof_event(sscater* h, hipEvent_t* out) {
     return hipSuccess;
 }
 
-// Launch wrapper: brackets the launch with events when profiling is enabled.
+// Launch wrapper: while profiling is enabled the launch carries two events
+// that its dispatch stamps at the kernel's start and end.
 template <class F>
 hipError_t timed_launch(sscater* h, int slot, hipStream_t s, F&& launch) {
-    if (!h->prof) return launch();
+    LaunchCtx c;
+    c.stream = s;
+    if (!h->prof) return launch(c);
     sscater::ProfRec r{slot, nullptr, nullptr};
     hipError_t e = prof_event(h, &r.a);
-    if (e == hipSuccess) e = hipEventRecord(r.a, s);
+    if (e == hipSuccess) e = prof_event(h, &r.b);
     if (e != hipSuccess) return e;
-    e = launch();
-    if (e != hipSuccess) return e;
-    e = prof_event(h, &r.b);
-    if (e == hipSuccess) e = hipEventRecord(r.b, s);
+    c.start = r.a;
+    c.stop = r.b;
+    e = launch(c);
     if (e == hipSuccess) h->prof_recs.push_back(r);
     return e;
 }
@@ -405,7 +407,7 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
     d.epoch = epoch;
     d.err = h->err_dev;
     d.next = prop_target(h, 1, set);
-    hipError_t e = timed_launch(h, 0, s, [&] { return launch_detect_present(d, h->row_bytes, h->bf16, s); });
+    hipError_t e = timed_launch(h, 0, s, [&](const LaunchCtx& c) { return launch_detect_present(d, h->row_bytes, h->bf16, c); });
     if (e != hipSuccess) return hip_fail(e);
 
     // vanished cells of the previous list, and the ownership check of the
@@ -420,7 +422,7 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
         v.prev_out = nullptr;
         v.zero_ptr = nullptr;
         v.zero_n = 0;
-        e = timed_launch(h, 1, s, [&] { return launch_detect_vanished(v, h->row_bytes, h->bf16, s); });
+        e = timed_launch(h, 1, s, [&](const LaunchCtx& c) { return launch_detect_vanished(v, h->row_bytes, h->bf16, c); });
         if (e != hipSuccess) return hip_fail(e);
     }
 
@@ -448,8 +450,8 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
             a.cum_dst = h->cum;
             a.n_cum = h->ncnt();
         }
-        e = timed_launch(h, 1 + l, s, [&] {
-            return launch_layer(a, ls.spec.cin, ls.spec.cout, ls.spec.stride, h->bf16, h->layer_grid, s);
+        e = timed_launch(h, 1 + l, s, [&](const LaunchCtx& c) {
+            return launch_layer(a, ls.spec.cin, ls.spec.cout, ls.spec.stride, h->bf16, h->layer_grid, c);
         });
         if (e != hipSuccess) return hip_fail(e);
     }
@@ -470,8 +472,8 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
         a.stamp = h->stamp_n;
         a.Wsrc = us.Ws;
         a.epoch = epoch;
-        e = timed_launch(h, h->L + 2 + u, s, [&] {
-            return launch_upsample(a, us.cin, us.spec.cout, us.spec.stride, h->bf16, h->layer_grid, s);
+        e = timed_launch(h, h->L + 2 + u, s, [&](const LaunchCtx& c) {
+            return launch_upsample(a, us.cin, us.spec.cout, us.spec.stride, h->bf16, h->layer_grid, c);
         });
         if (e != hipSuccess) return hip_fail(e);
     }

@@ -116,7 +116,7 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
 }
 
 template <bool VANISH>
-static hipError_t launch_detect(const DetectArgs& a, int row_bytes, bool bf16, hipStream_t s) {
+static hipError_t launch_detect(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c) {
     const int G = row_bytes / 16;
     const int ppw = 64 / G;
     const int rows = VANISH ? std::max(a.count, a.chk_count) : a.count;
@@ -127,9 +127,8 @@ static hipError_t launch_detect(const DetectArgs& a, int row_bytes, bool bf16, h
     dim3 grid((unsigned)blocks), block(256);
 #define SSC_DETECT_CASE(RB)                                                                      \
     case RB:                                                                                     \
-        if (bf16) hipLaunchKernelGGL((detect_kernel<RB, true, VANISH>), grid, block, 0, s, a);   \
-        else hipLaunchKernelGGL((detect_kernel<RB, false, VANISH>), grid, block, 0, s, a);       \
-        break;
+        return bf16 ? launch_kernel(c, detect_kernel<RB, true, VANISH>, grid, block, a)          \
+                    : launch_kernel(c, detect_kernel<RB, false, VANISH>, grid, block, a);
     switch (row_bytes) {
         SSC_DETECT_CASE(16)
         SSC_DETECT_CASE(32)
@@ -142,15 +141,14 @@ static hipError_t launch_detect(const DetectArgs& a, int row_bytes, bool bf16, h
             return hipErrorInvalidValue;
     }
 #undef SSC_DETECT_CASE
-    return hipGetLastError();
 }
 
-hipError_t launch_detect_present(const DetectArgs& a, int row_bytes, bool bf16, hipStream_t s) {
-    return launch_detect<false>(a, row_bytes, bf16, s);
+hipError_t launch_detect_present(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c) {
+    return launch_detect<false>(a, row_bytes, bf16, c);
 }
 
-hipError_t launch_detect_vanished(const DetectArgs& a, int row_bytes, bool bf16, hipStream_t s) {
-    return launch_detect<true>(a, row_bytes, bf16, s);
+hipError_t launch_detect_vanished(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c) {
+    return launch_detect<true>(a, row_bytes, bf16, c);
 }
 
 }  // namespace ssc

@@ -406,25 +406,25 @@ bool layer_supported(int cin, int cout, int stride, bool /*bf16*/) {
 }
 
 template <int CI, int CO, int S, bool BF16>
-static hipError_t launch_shape(const LayerArgs& a, int grid, hipStream_t s) {
+static hipError_t launch_shape(const LayerArgs& a, int grid, const LaunchCtx& c) {
     if constexpr (WideShape<CI, CO, BF16>::NCH > 4 && CO >= 32) {
         // tile pairs x cout groups x segments; at most ceil(cap / 32) pairs per segment
         constexpr int NH = WideShape<CI, CO, BF16>::NH;
         int gl = std::max(1, grid / (2 * NH * NSHARD));
         gl = std::min(gl, std::max(1, (a.cap + 31) / 32));
-        hipLaunchKernelGGL((layer_kernel_wide<CI, CO, S, BF16>), dim3(gl * NH * NSHARD), dim3(256), 0, s, a);
+        return launch_kernel(c, layer_kernel_wide<CI, CO, S, BF16>, dim3(gl * NH * NSHARD), dim3(256), a);
     } else {
         // whole runs of 4 tiles on every XCD for every segment
         grid = std::max(32 * NSHARD, grid / (32 * NSHARD) * (32 * NSHARD));
-        hipLaunchKernelGGL((layer_kernel<CI, CO, S, BF16>), dim3(grid), dim3(64 * LayerShape<CO>::NW), 0, s, a);
+        return launch_kernel(c, layer_kernel<CI, CO, S, BF16>, dim3(grid), dim3(64 * LayerShape<CO>::NW), a);
     }
-    return hipGetLastError();
 }
 
-hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, int grid, hipStream_t s) {
+hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, int grid,
+                        const LaunchCtx& c) {
 #define SSC_LAUNCH(CI, CO, S)                                                                               \
     if (cin == CI && cout == CO && stride == S)                                                             \
-        return bf16 ? launch_shape<CI, CO, S, true>(a, grid, s) : launch_shape<CI, CO, S, false>(a, grid, s);
+        return bf16 ? launch_shape<CI, CO, S, true>(a, grid, c) : launch_shape<CI, CO, S, false>(a, grid, c);
     SSC_ALL_SHAPES(SSC_LAUNCH)
 #undef SSC_LAUNCH
     return hipErrorInvalidValue;

@@ -2,6 +2,7 @@
 // Kernel arguments are plain structs passed by value.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -94,19 +95,35 @@ struct UpArgs {
 
 enum ErrBits { ERR_INDEX_RANGE = 1, ERR_DUPLICATE = 2 };
 
+// Where a launch goes: its stream and, while kernel timing is on, two events
+// that the dispatch packet itself stamps when the kernel starts and ends
+// (hipExtLaunchKernel), so no separate marker packets sit between kernels.
+struct LaunchCtx {
+    hipStream_t stream = nullptr;
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+
+template <class K, class A>
+inline hipError_t launch_kernel(const LaunchCtx& c, K kernel, dim3 grid, dim3 block, const A& args) {
+    if (c.start) hipExtLaunchKernelGGL(kernel, grid, block, 0, c.stream, c.start, c.stop, 0, args);
+    else hipLaunchKernelGGL(kernel, grid, block, 0, c.stream, args);
+    return hipGetLastError();
+}
+
 // Host-side launchers (defined in the kernel translation units).
-hipError_t launch_detect_present(const DetectArgs& a, int row_bytes, bool bf16, hipStream_t s);
-hipError_t launch_detect_vanished(const DetectArgs& a, int row_bytes, bool bf16, hipStream_t s);
+hipError_t launch_detect_present(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c);
+hipError_t launch_detect_vanished(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c);
 bool layer_supported(int cin, int cout, int stride, bool bf16);
 hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, int grid,
-                        hipStream_t s);
+                        const LaunchCtx& c);
 hipError_t launch_read(const float* Z, void* dst, long long n, int relu, bool bf16, hipStream_t s);
 // phi of channels [coff, coff + cout) of a [cells][ctot] map into the same
 // channels of a [cells][ctot] destination.
 hipError_t launch_read_slice(const float* Z, void* dst, long long cells, int ctot, int coff, int cout, int relu,
                              bool bf16, hipStream_t s);
 bool upsample_supported(int cin, int cout, int stride);
-hipError_t launch_upsample(const UpArgs& a, int cin, int cout, int stride, bool bf16, int grid, hipStream_t s);
+hipError_t launch_upsample(const UpArgs& a, int cin, int cout, int stride, bool bf16, int grid,
+                           const LaunchCtx& c);
 size_t up_wpack_elems(int cin, int cout, int stride, bool bf16);
 // Repack [cin][cout][S][S] transposed-conv weights (fp32 values, or bf16 bits)
 // into the layout the upsampling kernel reads.

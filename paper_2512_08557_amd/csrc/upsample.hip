@@ -138,19 +138,19 @@ bool upsample_supported(int cin, int cout, int stride) {
 }
 
 template <int CI, int CO, int S, bool BF16>
-static hipError_t launch_up_shape(const UpArgs& a, int grid, hipStream_t s) {
+static hipError_t launch_up_shape(const UpArgs& a, int grid, const LaunchCtx& c) {
     using U = UpShape<CI, CO, S, BF16>;
     // tile slots per (segment, block group); at most ceil(cap / 16) tiles per segment
     int tg = std::max(1, grid / (U::OBG * NSHARD));
     tg = std::min(tg, std::max(1, (a.cap + 15) / 16));
-    hipLaunchKernelGGL((upsample_kernel<CI, CO, S, BF16>), dim3(tg * U::OBG * NSHARD), dim3(256), 0, s, a);
-    return hipGetLastError();
+    return launch_kernel(c, upsample_kernel<CI, CO, S, BF16>, dim3(tg * U::OBG * NSHARD), dim3(256), a);
 }
 
-hipError_t launch_upsample(const UpArgs& a, int cin, int cout, int stride, bool bf16, int grid, hipStream_t s) {
+hipError_t launch_upsample(const UpArgs& a, int cin, int cout, int stride, bool bf16, int grid,
+                           const LaunchCtx& c) {
 #define SSC_LAUNCH(CI, CO, S)                                                                               \
     if (cin == CI && cout == CO && stride == S)                                                             \
-        return bf16 ? launch_up_shape<CI, CO, S, true>(a, grid, s) : launch_up_shape<CI, CO, S, false>(a, grid, s);
+        return bf16 ? launch_up_shape<CI, CO, S, true>(a, grid, c) : launch_up_shape<CI, CO, S, false>(a, grid, c);
     SSC_UP_SHAPES(SSC_LAUNCH)
 #undef SSC_LAUNCH
     return hipErrorInvalidValue;
