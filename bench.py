@@ -257,6 +257,82 @@ def copy_calibration(nbytes: int) -> int:
     return 0
 
 
+def run_sweep(K: int, W: int, n_full: int) -> dict:
+    """Single-layer channel sweep (the shapes of the paper's single-layer
+    timing tables, Sec. IV-B, Tables I and II) on the 504 x 504 drone stream:
+    per shape the delta stride (wall clock over K strides), the layer kernel
+    alone (dispatch-stamped events), and the full recompute of the same
+    windows through the same kernels (reset + one pass over every active
+    pillar, the scatter conv without recycling)."""
+    import torch
+    from paper_2512_08557_amd import Engine
+
+    rows = []
+    stream = torch.cuda.current_stream()
+    for ci in S.SWEEP_CIN:
+        for co in S.SWEEP_COUT:
+            wl = S.workload(f"l{ci}x{co}")
+            strides = S.make_stream(wl.name, n_strides=W + K)
+            dev = upload(strides, wl.dtype)
+            eng = Engine(wl.H, wl.W, wl.C0, layers_of(wl), S.weights(wl.name), dtype=wl.dtype,
+                         max_pillars=wl.max_pillars)
+            for k in range(1 + W):
+                eng.step(*dev[k])
+            torch.cuda.synchronize()
+            before = eng.stats()
+            t0 = time.perf_counter()
+            for k in range(1 + W, 1 + W + K):
+                eng.step(*dev[k])
+            torch.cuda.synchronize()
+            wall_ms = (time.perf_counter() - t0) * 1e3
+            after = eng.stats()
+            a_in = after["active_total"][0] - before["active_total"][0]
+            a_out = after["active_total"][1] - before["active_total"][1]
+            pairs = after["pairs_total"][1] - before["pairs_total"][1]
+            # per-kernel pass over the same strides
+            eng.reset()
+            for k in range(1 + W):
+                eng.step(*dev[k])
+            eng.profile_read()
+            eng.profile(True)
+            for k in range(1 + W, 1 + W + K):
+                eng.step(*dev[k])
+            ms, cnt = eng.profile_read()
+            eng.profile(False)
+            # full recompute of n_full windows spread over the timed range
+            full = []
+            for k in range(1 + W, 1 + W + K, max(1, K // n_full)):
+                eng.reset()
+                torch.cuda.synchronize()
+                a = torch.cuda.Event(enable_timing=True)
+                b = torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                eng.step(*dev[k])
+                b.record(stream)
+                torch.cuda.synchronize()
+                full.append(a.elapsed_time(b))
+            eng.close()
+            ms_stride = wall_ms / K
+            full_ms = statistics.fmean(full)
+            layer_us = ms[2] / cnt[2] * 1e3
+            rows.append({"cin": ci, "cout": co, "ms_per_stride": ms_stride, "layer_kernel_us": layer_us,
+                         "detect_us": (ms[0] + ms[1]) / K * 1e3, "full_recompute_ms": full_ms,
+                         "speedup_vs_full_recompute": full_ms / ms_stride,
+                         "updates_per_s": a_in / (wall_ms / 1e3),
+                         "layer_tflops": 2.0 * ci * co * pairs / (ms[2] / 1e3) / 1e12,
+                         "mean_changed_in": a_in / K, "mean_changed_out": a_out / K,
+                         "mean_pillars": float(np.mean([len(x.idx) for x in strides[1 + W:]]))})
+            r = rows[-1]
+            log(f"[sweep] {ci:4d} -> {co:4d}: {ms_stride * 1e3:7.1f} us/stride (layer {layer_us:6.1f} us, "
+                f"{r['layer_tflops']:5.2f} TFLOP/s), full recompute {full_ms * 1e3:7.1f} us, "
+                f"x{r['speedup_vs_full_recompute']:.2f}; |A_0| {r['mean_changed_in']:.0f}, "
+                f"|A_1| {r['mean_changed_out']:.0f}")
+    return {"metric": "single-layer sweep: ms per stride, layer kernel us, full recompute ms", "n_gpus": 1,
+            "steps": K, "warmup": W, "dtype": "f32", "data": "synthetic",
+            "config": {"workload": "single 3x3 s1 conv (ReLU), Cin 16..128 x Cout 8..128, 504x504 drone scan"},
+            "rows": rows}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -268,6 +344,8 @@ def main() -> int:
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
     ap.add_argument("--no-full", action="store_true", help="skip the GPU full-recompute timing")
     ap.add_argument("--neck", action="store_true", help="include the upsampling neck (c3, c4)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="single-layer channel sweep over all 20 (Cin, Cout) shapes on the 504x504 drone stream")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="only run a plain device copy of this many bytes (counter calibration)")
     ap.add_argument("--digest-trace", metavar="CSV", help="summarise a rocprofv3 kernel-trace csv and exit")
@@ -301,6 +379,9 @@ def main() -> int:
     from paper_2512_08557_amd import Engine
 
     torch.cuda.set_device(0)
+    if args.sweep:
+        print(json.dumps(run_sweep(args.steps, args.warmup, 10)), flush=True)
+        return 0
     wl = S.workload(args.workload)
     ws = S.weights(args.workload)
     K, W = args.steps, args.warmup

@@ -46,9 +46,11 @@
 
 namespace ssc {
 
+// COUT = 8 takes one 16-wide block whose upper 8 weight rows are zero; the
+// lanes holding those rows (k-groups 2 and 3) neither read nor write Z.
 template <int COUT>
 struct LayerShape {
-    static constexpr int NCBT = COUT / 16;                  // 16-wide cout blocks
+    static constexpr int NCBT = (COUT + 15) / 16;           // 16-wide cout blocks
     static constexpr int NW = NCBT >= 4 ? 4 : NCBT;         // wavefronts per workgroup
     static constexpr int NCB = NCBT / NW;                   // cout blocks per wavefront
 };
@@ -166,7 +168,8 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
         float* zrow = a.Z + (size_t)q * COUT;
         f4v zo[NCB];
 #pragma unroll
-        for (int cb = 0; cb < NCB; ++cb) zo[cb] = *reinterpret_cast<const f4v*>(zrow + (wave * NCB + cb) * 16 + 4 * g);
+        for (int cb = 0; cb < NCB; ++cb)
+            zo[cb] = *reinterpret_cast<const f4v*>(zrow + min((wave * NCB + cb) * 16 + 4 * g, COUT - 4));
         // next layer's change list: stamp the footprint in the same round trip
         // as the stamp and map loads, append the new cells at the end
         PropBatch<4> pb;
@@ -253,7 +256,10 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
 
         if (vrow) {
 #pragma unroll
-            for (int cb = 0; cb < NCB; ++cb) epilogue4<COUT, BF16>(a, q, (wave * NCB + cb) * 16 + 4 * g, zo[cb], acc[cb]);
+            for (int cb = 0; cb < NCB; ++cb) {
+                const int co0 = (wave * NCB + cb) * 16 + 4 * g;
+                if (COUT % 16 == 0 || co0 < COUT) epilogue4<COUT, BF16>(a, q, co0, zo[cb], acc[cb]);
+            }
         }
         if (do_prop) prop_finish<4>(a.next, a.epoch, shard, pb);
 
@@ -392,7 +398,7 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
 // ---------------------------------------------------------------------------
 // instantiation table
 // ---------------------------------------------------------------------------
-#define SSC_CH_LIST(X, CIN, S) X(CIN, 16, S) X(CIN, 32, S) X(CIN, 64, S) X(CIN, 128, S) X(CIN, 256, S)
+#define SSC_CH_LIST(X, CIN, S) X(CIN, 8, S) X(CIN, 16, S) X(CIN, 32, S) X(CIN, 64, S) X(CIN, 128, S) X(CIN, 256, S)
 #define SSC_ALL_SHAPES(X)                                                                            \
     SSC_CH_LIST(X, 16, 1) SSC_CH_LIST(X, 32, 1) SSC_CH_LIST(X, 64, 1) SSC_CH_LIST(X, 128, 1)         \
     SSC_CH_LIST(X, 256, 1) SSC_CH_LIST(X, 16, 2) SSC_CH_LIST(X, 32, 2) SSC_CH_LIST(X, 64, 2)         \
@@ -434,15 +440,16 @@ hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool 
 // weight repacking (host)
 // ---------------------------------------------------------------------------
 size_t wpack_elems(int cin, int cout, bool bf16) {
-    return (size_t)9 * (size_t)(bf16 ? 2 * cin : cin) * (size_t)cout;
+    return (size_t)9 * (size_t)(bf16 ? 2 * cin : cin) * (size_t)((cout + 15) / 16 * 16);
 }
 
 // Layout, in 16-byte lane vectors: [tap t][chunk c][cout block cb][lane l],
 // lane l of block cb holds output channel cb*16 + l%16 and the k-group l/16 of
 // chunk c: fp32 k = c*16 + 4*(l/16) + e (e < 4); bf16 k = c*32 + 8*(l/16) + e
-// (e < 8) over the pair [W | -W].
+// (e < 8) over the pair [W | -W].  Output channels past cout (cout = 8) are
+// zero.
 void pack_weights(const void* w_oihw, int cin, int cout, bool bf16, void* dst) {
-    const int ncbt = cout / 16;
+    const int ncbt = (cout + 15) / 16;
     if (!bf16) {
         const float* w = static_cast<const float*>(w_oihw);
         float* out = static_cast<float*>(dst);
@@ -455,7 +462,7 @@ void pack_weights(const void* w_oihw, int cin, int cout, bool bf16, void* dst) {
                             const int co = cb * 16 + l % 16;
                             const int ci = c * 16 + 4 * (l / 16) + e;
                             out[((((size_t)t * nch + c) * ncbt + cb) * 64 + l) * 4 + e] =
-                                w[(((size_t)co * cin + ci) * 3 + t / 3) * 3 + t % 3];
+                                co < cout ? w[(((size_t)co * cin + ci) * 3 + t / 3) * 3 + t % 3] : 0.f;
                         }
     } else {
         const uint16_t* w = static_cast<const uint16_t*>(w_oihw);
@@ -469,8 +476,8 @@ void pack_weights(const void* w_oihw, int cin, int cout, bool bf16, void* dst) {
                             const int co = cb * 16 + l % 16;
                             const int k = c * 32 + 8 * (l / 16) + e;
                             const int ci = k < cin ? k : k - cin;
-                            uint16_t v = w[(((size_t)co * cin + ci) * 3 + t / 3) * 3 + t % 3];
-                            if (k >= cin) v ^= 0x8000u;   // -W: exact sign flip
+                            uint16_t v = co < cout ? w[(((size_t)co * cin + ci) * 3 + t / 3) * 3 + t % 3] : 0;
+                            if (k >= cin) v ^= 0x8000u;   // -W: exact sign flip (-0 for the padding)
                             out[((((size_t)t * nch + c) * ncbt + cb) * 64 + l) * 8 + e] = v;
                         }
     }

@@ -39,7 +39,7 @@ WEIGHT_SEED = 8557
 __all__ = [
     "LayerSpec", "Workload", "workload", "WORKLOADS", "weights", "make_stream", "UpSpec", "neck", "neck_weights",
     "Stream", "Stride", "round_to_bf16_bits", "bf16_bits_to_f32", "out_shape",
-    "cell_azimuth_sector",
+    "cell_azimuth_sector", "SWEEP_CIN", "SWEEP_COUT",
 ]
 
 
@@ -76,6 +76,24 @@ def _block(cin: int, f: int, n: int) -> List[LayerSpec]:
 
 _BACKBONE = tuple(_block(64, 64, 4) + _block(64, 128, 6) + _block(128, 256, 6))
 
+# Single-layer channel sweep at the paper's drone-LiDAR sparsity: one 3x3
+# stride-1 conv, Cin in {16, 32, 64, 128} x Cout in {8, 16, 32, 64, 128}, on a
+# 504 x 504 grid of 0.16 m pillars (the shapes of the single-layer timing
+# tables, Sec. IV-B, Tables I and II).
+SWEEP_CIN = (16, 32, 64, 128)
+SWEEP_COUT = (8, 16, 32, 64, 128)
+
+
+def _sweep_workloads() -> dict:
+    out = {}
+    for ci in SWEEP_CIN:
+        for co in SWEEP_COUT:
+            name = f"l{ci}x{co}"
+            out[name] = Workload(name, 504, 504, ci, "f32", (LayerSpec(ci, co, 1, True),), 100, 4096,
+                                 f"single 3x3 s1 conv {ci}->{co} (ReLU), 504x504 forward-looking drone scan")
+    return out
+
+
 WORKLOADS = {
     "c1": Workload("c1", 64, 64, 16, "f32", (LayerSpec(16, 16, 1, False),), 10, 4096,
                    "single 3x3 s1 conv 16->16, 64x64 grid, no ReLU"),
@@ -87,7 +105,13 @@ WORKLOADS = {
                    "3-block backbone in bf16 (fp32 accumulate), 18 deg strides + 1% toggles"),
     "c5": Workload("c5", 1024, 1024, 64, "f32", tuple(_block(64, 64, 4)), 100, 48000,
                    "1024x1024 drone grid, block 1, 4 concurrent streams"),
+    **_sweep_workloads(),
 }
+
+
+def _family(name: str) -> int:
+    """Seed family of a workload: c1..c5 -> 1..5, the single-layer sweep -> 6."""
+    return 6 if name.startswith("l") else int(name[1])
 
 
 def workload(name: str) -> Workload:
@@ -155,16 +179,17 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
 def weights(name: str) -> List[np.ndarray]:
     """Per-layer OIHW float32 weights.
 
-    c1: N(0, 1/144).  c2..c5: He-normal N(0, 2/(9*cin)).  c2/c3/c4 share the
+    c1: N(0, 1/144).  c2..c5 and the sweep: He-normal N(0, 2/(9*cin)).  c2/c3/c4 share the
     432x496 backbone family, so c2's four layers equal c3's first four; c4 is
     c3 rounded to bfloat16 (returned as float32 values that are exactly
     representable in bfloat16).
     """
     wl = workload(name)
-    family = {"c1": 1, "c2": 2, "c3": 2, "c4": 2, "c5": 5}[name]
+    family = {"c1": 1, "c2": 2, "c3": 2, "c4": 2, "c5": 5}.get(name, 6)
     out = []
     for li, ls in enumerate(wl.layers):
-        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence((WEIGHT_SEED, family, li))))
+        key = (WEIGHT_SEED, family, li) if family != 6 else (WEIGHT_SEED, family, ls.cin, ls.cout)
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence(key)))
         std = (1.0 / 12.0) if name == "c1" else math.sqrt(2.0 / (9.0 * ls.cin))
         w = (rng.standard_normal((ls.cout, ls.cin, 3, 3)) * std).astype(np.float32)
         if wl.dtype == "bf16":
@@ -221,6 +246,38 @@ def _box_perimeter(cx, cy, a, b, yaw, H, W, res) -> np.ndarray:
     return _metres_to_cells(xs, ys, H, W, res)
 
 
+# Forward-looking drone LiDAR with a non-repeating rosette scan (the stand-in
+# for the paper's drone datasets, Sec. III-A): 24,000 emitted beams per
+# 100 ms, of which a minority return; active and changed cells per 10 ms stride
+# come out near the means the paper reports for its 504 x 504 grid (1,781
+# active, 483 changed, 27 %; Sec. IV-A).
+_SCAN_BEAMS = 2400              # emitted beams per 10 ms stride
+_SCAN_PRISM_HZ = (457.3, -319.9)  # two counter-rotating prisms ...
+_SCAN_PRISM_DEG = 15.0          # ... each deflecting by 15 degrees: a 60 degree cone
+_SCAN_ALT_M = 10.0              # sensor height above flat ground
+_SCAN_PITCH_DEG = 45.0          # boresight below the horizon
+_SCAN_SPEED = 3.0               # forward speed, m/s
+_SCAN_X0 = -20.0                # sensor position relative to the grid centre at t = 0, m
+_SCAN_RETURN = 0.12             # mean return probability of a beam that reaches the ground
+_SCAN_RETURN_SWING = 0.4        # +-40 % over a 40-stride period (surfaces come and go)
+
+
+def _rosette_hits(rng: np.random.Generator, s: int, H: int, W: int, res: float) -> np.ndarray:
+    """Unique cells hit by the returns of 10 ms stride s (s may be negative)."""
+    T = 0.01
+    t = s * T + np.arange(_SCAN_BEAMS) * (T / _SCAN_BEAMS)
+    d = math.radians(_SCAN_PRISM_DEG)
+    w1, w2 = 2.0 * math.pi * _SCAN_PRISM_HZ[0], 2.0 * math.pi * _SCAN_PRISM_HZ[1]
+    az = d * (np.cos(w1 * t) + np.cos(w2 * t))           # beam offset from the boresight
+    el = -math.radians(_SCAN_PITCH_DEG) + d * (np.sin(w1 * t) + np.sin(w2 * t))
+    p = _SCAN_RETURN * (1.0 + _SCAN_RETURN_SWING * math.sin(2.0 * math.pi * s / 40.0))
+    keep = (el < -1e-3) & (rng.random(_SCAN_BEAMS) < p)   # below the horizon, and returned
+    rng_m = _SCAN_ALT_M / np.tan(-el[keep])               # ground range
+    x = rng_m * np.cos(az[keep]) + _SCAN_X0 + _SCAN_SPEED * t[keep]
+    y = rng_m * np.sin(az[keep])
+    return _metres_to_cells(x, y, H, W, res)
+
+
 def _thin(cells: np.ndarray, target: int, rng: np.random.Generator) -> np.ndarray:
     if cells.size <= target:
         return cells
@@ -260,6 +317,9 @@ class Stream:
         elif name == "c5":
             occ = self._scene_1024(scene_rng)
             self.n_sectors = 20
+        elif _family(name) == 6:
+            occ = self._scene_drone_scan(seed)
+            self.n_sectors = 1
         else:
             raise ValueError(name)
         self.sector = cell_azimuth_sector(wl.H, wl.W, self.n_sectors)
@@ -289,6 +349,17 @@ class Stream:
         cells = np.unique(np.concatenate([ground] + boxes))
         return np.sort(_thin(cells, 12000, rng))
 
+    def _scene_drone_scan(self, seed: int) -> np.ndarray:
+        """Cells hit in every stride -9..n (the window of stride s is the ten
+        strides s-9..s); the initial window's occupied cells."""
+        H, W, res = self.wl.H, self.wl.W, 0.16
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence((seed, 6, 0))))
+        self._hits = [_rosette_hits(rng, s, H, W, res) for s in range(-9, self.n_strides + 1)]
+        self._wcount = np.zeros(H * W, dtype=np.int16)     # strides of the window that hit each cell
+        for h in self._hits[:10]:
+            self._wcount[h] += 1
+        return np.flatnonzero(self._wcount)
+
     def _scene_1024(self, rng) -> np.ndarray:
         H, W, res = 1024, 1024, 0.1
         ground = _rings(H, W, res, 40, 2.0, 70.0)
@@ -315,7 +386,7 @@ class Stream:
 
     # -- per-stride randomness ----------------------------------------------
     def _stride_rng(self, s: int) -> np.random.Generator:
-        cfg = int(self.name[1])
+        cfg = _family(self.name)
         return np.random.Generator(np.random.PCG64(np.random.SeedSequence((self.seed, cfg, s + 1))))
 
     def _fill(self, cells: np.ndarray, rng) -> None:
@@ -346,6 +417,20 @@ class Stream:
             self._fill(on, rng)
         elif self.name in ("c2", "c3"):
             self._fill(np.flatnonzero(self.occ & in_sec), rng)
+        elif _family(self.name) == 6:
+            # a cell changes when the new stride hits it or the expiring one
+            # (stride s-10) did; it stays occupied while any stride of the
+            # window hits it, with a fresh feature vector
+            new, old = self._hits[s + 9], self._hits[s - 1]
+            self._wcount[new] += 1
+            self._wcount[old] -= 1
+            changed = np.union1d(new, old)
+            live = self._wcount[changed] > 0
+            off, on = changed[~live], changed[live]
+            self.occ[off] = False
+            self.feat[off] = 0.0
+            self.occ[on] = True
+            self._fill(on, rng)
         elif self.name == "c4":
             self._fill(np.flatnonzero(self.occ & in_sec), rng)
             occ_sec = np.flatnonzero(self.occ & in_sec)

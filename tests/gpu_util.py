@@ -66,6 +66,54 @@ def check_maps(eng, ys_ref, tol, where=""):
             assert err <= tol * scale, f"{where} layer {l}: max err {err:.3e} > {tol} * {scale:.3e}"
 
 
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def oracle_maps(stride, wl, ws):
+    x = oracle.exact_canvas(S.canvas(stride, wl.H, wl.W, wl.C0), wl.dtype)
+    return oracle.forward(x, ws, layers_of(wl), bf16_storage=(wl.dtype == "bf16"))
+
+
+def run_stream(name, n_strides=None, map_every=10, list_every=1):
+    wl = S.workload(name)
+    ws = S.weights(name)
+    strides = S.make_stream(name, n_strides=n_strides)
+    dev = [to_device(s, wl.dtype) for s in strides]
+    eng = make_engine(wl, ws)
+    prev_bits = np.zeros((wl.H, wl.W, wl.C0), dtype=np.uint16 if wl.dtype == "bf16" else np.uint32)
+    strides_l = [l.stride for l in wl.layers]
+    last = len(strides) - 1
+    worst = [0.0] * len(wl.layers)
+    for t, (st, (idx, feats)) in enumerate(zip(strides, dev)):
+        note(f"[gpu-test] {name} stride {t} P={len(st.idx)}")
+        eng.step(idx, feats)
+        bits = canvas_bits(st, wl)
+        if t % list_every == 0 or t == last:
+            ref_lists = oracle.changed_lists(prev_bits, bits, strides_l)
+            check_lists(eng, ref_lists, f"{name} stride {t}")
+            stt = eng.stats()
+            assert stt["active"] == [len(a) for a in ref_lists]
+            masks = [np.isin(np.arange(wl.H * wl.W), ref_lists[0]).reshape(wl.H, wl.W)]
+            for l, ls in enumerate(wl.layers):
+                h, w = masks[-1].shape
+                assert stt["pairs"][l + 1] == oracle.pair_counts(masks[-1], ls.stride), f"pairs layer {l + 1}"
+                m = np.zeros(((h - 1) // ls.stride + 1, (w - 1) // ls.stride + 1), dtype=bool)
+                m.flat[ref_lists[l + 1]] = True
+                masks.append(m)
+        if t % map_every == 0 or t == last:
+            ys = oracle_maps(st, wl, ws)
+            errs = map_errors(eng, ys)
+            for l, (e, sc) in enumerate(errs):
+                worst[l] = max(worst[l], e / sc if sc else e)
+            check_maps(eng, ys, TOL[wl.dtype], f"{name} stride {t}")
+            x0 = read_map(eng, 0)
+            np.testing.assert_array_equal(x0, oracle.exact_canvas(S.canvas(st, wl.H, wl.W, wl.C0), wl.dtype))
+        prev_bits = bits
+    note(f"[gpu-test] {name} worst relative map error per layer: {['%.2e' % w for w in worst]}")
+    eng.close()
+    return worst
+
+
 def note(msg):
     sys.stderr.write(msg + "\n")
     sys.stderr.flush()

@@ -9,8 +9,8 @@ import pytest
 
 import oracle
 import streams as S
-from gpu_util import (canvas_bits, check_lists, check_maps, layers_of, make_engine, map_errors, note, read_map,
-                      to_device)
+from gpu_util import (canvas_bits, check_lists, check_maps, layers_of, make_engine, note, oracle_maps, read_map,
+                      run_stream, to_device)
 
 pytestmark = pytest.mark.gpu
 
@@ -28,65 +28,20 @@ def _announce(request):
     torch.cuda.synchronize()
 
 
-def _oracle_maps(stride, wl, ws):
-    x = oracle.exact_canvas(S.canvas(stride, wl.H, wl.W, wl.C0), wl.dtype)
-    return oracle.forward(x, ws, layers_of(wl), bf16_storage=(wl.dtype == "bf16"))
-
-
-def _run_stream(name, n_strides=None, map_every=10, list_every=1):
-    wl = S.workload(name)
-    ws = S.weights(name)
-    strides = S.make_stream(name, n_strides=n_strides)
-    dev = [to_device(s, wl.dtype) for s in strides]
-    eng = make_engine(wl, ws)
-    prev_bits = np.zeros((wl.H, wl.W, wl.C0), dtype=np.uint16 if wl.dtype == "bf16" else np.uint32)
-    strides_l = [l.stride for l in wl.layers]
-    last = len(strides) - 1
-    worst = [0.0] * len(wl.layers)
-    for t, (st, (idx, feats)) in enumerate(zip(strides, dev)):
-        note(f"[gpu-test] {name} stride {t} P={len(st.idx)}")
-        eng.step(idx, feats)
-        bits = canvas_bits(st, wl)
-        if t % list_every == 0 or t == last:
-            ref_lists = oracle.changed_lists(prev_bits, bits, strides_l)
-            check_lists(eng, ref_lists, f"{name} stride {t}")
-            stt = eng.stats()
-            assert stt["active"] == [len(a) for a in ref_lists]
-            masks = [np.isin(np.arange(wl.H * wl.W), ref_lists[0]).reshape(wl.H, wl.W)]
-            for l, ls in enumerate(wl.layers):
-                h, w = masks[-1].shape
-                assert stt["pairs"][l + 1] == oracle.pair_counts(masks[-1], ls.stride), f"pairs layer {l + 1}"
-                m = np.zeros(((h - 1) // ls.stride + 1, (w - 1) // ls.stride + 1), dtype=bool)
-                m.flat[ref_lists[l + 1]] = True
-                masks.append(m)
-        if t % map_every == 0 or t == last:
-            ys = _oracle_maps(st, wl, ws)
-            errs = map_errors(eng, ys)
-            for l, (e, sc) in enumerate(errs):
-                worst[l] = max(worst[l], e / sc if sc else e)
-            check_maps(eng, ys, TOL[wl.dtype], f"{name} stride {t}")
-            x0 = read_map(eng, 0)
-            np.testing.assert_array_equal(x0, oracle.exact_canvas(S.canvas(st, wl.H, wl.W, wl.C0), wl.dtype))
-        prev_bits = bits
-    note(f"[gpu-test] {name} worst relative map error per layer: {['%.2e' % w for w in worst]}")
-    eng.close()
-    return worst
-
-
 def test_c1_single_layer_all_strides():
-    _run_stream("c1", map_every=1)
+    run_stream("c1", map_every=1)
 
 
 def test_c2_block1_100_strides():
-    _run_stream("c2", map_every=10)
+    run_stream("c2", map_every=10)
 
 
 def test_c3_backbone_100_strides():
-    _run_stream("c3", map_every=25)
+    run_stream("c3", map_every=25)
 
 
 def test_c4_backbone_bf16_200_strides():
-    _run_stream("c4", map_every=50)
+    run_stream("c4", map_every=50)
 
 
 def test_c5_four_concurrent_streams():
@@ -112,7 +67,7 @@ def test_c5_four_concurrent_streams():
                 hip_streams[k].synchronize()
                 bits = canvas_bits(sts[k], wl)
                 check_lists(engs[k], oracle.changed_lists(prev[k], bits, strides_l), f"c5[{k}] stride {t}")
-                check_maps(engs[k], _oracle_maps(sts[k], wl, ws), TOL["f32"], f"c5[{k}] stride {t}")
+                check_maps(engs[k], oracle_maps(sts[k], wl, ws), TOL["f32"], f"c5[{k}] stride {t}")
         else:
             for k in range(4):
                 hip_streams[k].synchronize()
@@ -273,6 +228,9 @@ STACKS = [
     (40, 3, 16, [(16, 16, 2, True)] * 4, "f32"),
     (13, 21, 16, [(16, 32, 1, True), (32, 32, 2, True), (32, 64, 1, False)], "bf16"),
     (33, 29, 64, [(64, 64, 2, True), (64, 128, 1, True)], "bf16"),
+    (19, 23, 32, [(32, 8, 1, True)], "f32"),
+    (21, 17, 128, [(128, 8, 2, False)], "f32"),
+    (15, 26, 16, [(16, 8, 1, True)], "bf16"),
 ]
 
 

@@ -48,3 +48,41 @@ def test_weights_shapes_and_family():
     for a, b in zip(w2, w3):
         np.testing.assert_array_equal(a, b)
     assert w3[-1].shape == (256, 256, 3, 3)
+
+
+def _changed_count(prev, cur):
+    """Cells whose pillar appeared, vanished or carries a different vector."""
+    a = dict(zip(prev.idx.tolist(), range(len(prev.idx))))
+    n = len(set(prev.idx.tolist()) ^ set(cur.idx.tolist()))
+    for i, p in enumerate(cur.idx.tolist()):
+        j = a.get(p)
+        if j is not None and not np.array_equal(prev.feats[j], cur.feats[i]):
+            n += 1
+    return n
+
+
+def test_drone_scan_stream_has_the_paper_sparsity():
+    """Sweep stream on 504 x 504: the paper reports 1,781 active and 483
+    changed cells per 10 ms stride on average (27 % of active), with active
+    between 1,552 and 2,533 and changed between 169 and 1,154."""
+    st = S.make_stream("l64x64")
+    assert len(st) == 101
+    act = np.array([len(s.idx) for s in st[1:]])
+    chg = np.array([_changed_count(a, b) for a, b in zip(st, st[1:])])
+    assert 1600 < act.mean() < 2050 and act.min() > 1000 and act.max() < 2700
+    assert 420 < chg.mean() < 550 and chg.min() > 150 and chg.max() < 1200
+    assert 0.22 < (chg / act).mean() < 0.32
+    for s in st:
+        assert np.all(np.diff(s.idx) > 0) and np.all(np.any(s.feats != 0.0, axis=1))
+
+
+def test_sweep_streams_share_cells_and_differ_in_width():
+    a = S.make_stream("l16x8", n_strides=5)
+    b = S.make_stream("l128x64", n_strides=5)
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x.idx, y.idx)
+        assert x.feats.shape[1] == 16 and y.feats.shape[1] == 128
+    assert len(S.SWEEP_CIN) * len(S.SWEEP_COUT) == 20
+    w = S.weights("l32x8")
+    assert len(w) == 1 and w[0].shape == (8, 32, 3, 3)
+    assert not np.array_equal(S.weights("l32x16")[0][:8], w[0])
