@@ -48,11 +48,17 @@ namespace ssc {
 
 // COUT = 8 takes one 16-wide block whose upper 8 weight rows are zero; the
 // lanes holding those rows (k-groups 2 and 3) neither read nor write Z.
+// NWC wavefronts cover the cout blocks; with a single block (COUT <= 16)
+// KS = 4 wavefronts split the contraction (the (tap, chunk) steps) and add
+// their partial sums through LDS (measured: a 2-way split at COUT = 32 is
+// slower than 2 wavefronts with the whole contraction each).
 template <int COUT>
 struct LayerShape {
     static constexpr int NCBT = (COUT + 15) / 16;           // 16-wide cout blocks
-    static constexpr int NW = NCBT >= 4 ? 4 : NCBT;         // wavefronts per workgroup
-    static constexpr int NCB = NCBT / NW;                   // cout blocks per wavefront
+    static constexpr int NWC = NCBT >= 4 ? 4 : NCBT;        // wavefronts across the cout blocks
+    static constexpr int KS = NWC == 1 ? 4 : 1;             // wavefronts across the contraction
+    static constexpr int NW = NWC * KS;                     // wavefronts per workgroup
+    static constexpr int NCB = NCBT / NWC;                  // cout blocks per wavefront
 };
 
 // One 16-channel (fp32) or 32-value (bf16 pair) chunk of the contraction for
@@ -115,14 +121,16 @@ template <int CIN, int COUT, int S, bool BF16>
 __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerArgs a) {
     constexpr int NCBT = LayerShape<COUT>::NCBT;
     constexpr int NCB = LayerShape<COUT>::NCB;
+    constexpr int NWC = LayerShape<COUT>::NWC, KS = LayerShape<COUT>::KS;
     constexpr int KTOT = BF16 ? 2 * CIN : CIN;   // contraction length per tap
     constexpr int KCH = BF16 ? 32 : 16;          // k per 64-byte chunk
     constexpr int NCH = KTOT / KCH;
     constexpr int ROWB_IN = 4 * CIN;             // input delta row bytes (fp32, or bf16 pair)
     constexpr int ROWB_OUT = 4 * COUT;
 
-    const int lane = (int)(threadIdx.x & 63u), wave = (int)(threadIdx.x >> 6);
+    const int lane = (int)(threadIdx.x & 63u), wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int cl = lane & 15, g = lane >> 4;
+    const int cw = wave % NWC, ks = wave / NWC;  // cout group, contraction share
     const int G = (int)gridDim.x;                // a multiple of 32 * NSHARD
 
     // tiles of segment (b / 8) % NSHARD, first one without waiting for the
@@ -169,7 +177,7 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
         f4v zo[NCB];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb)
-            zo[cb] = *reinterpret_cast<const f4v*>(zrow + min((wave * NCB + cb) * 16 + 4 * g, COUT - 4));
+            zo[cb] = *reinterpret_cast<const f4v*>(zrow + min((cw * NCB + cb) * 16 + 4 * g, COUT - 4));
         // next layer's change list: stamp the footprint in the same round trip
         // as the stamp and map loads, append the new cells at the end
         PropBatch<4> pb;
@@ -183,7 +191,7 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
         }
 
         const char* dbase = static_cast<const char*>(a.delta_in) + g * 16;
-        const uint4* wbase = static_cast<const uint4*>(a.wpack) + (size_t)wave * NCB * 64 + lane;
+        const uint4* wbase = static_cast<const uint4*>(a.wpack) + (size_t)cw * NCB * 64 + lane;
         f4v acc[NCB];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) acc[cb] = f4v{0.f, 0.f, 0.f, 0.f};
@@ -208,56 +216,84 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
                 }
             }
         };
-        if constexpr (NCH <= 4) {
-            // narrow inputs: the 9 * NCH (tap, chunk) steps are fully unrolled
-            // and both operands are prefetched PF steps ahead, so the weight
-            // and delta loads of later taps overlap the current MFMAs
-            constexpr int NSTEP = 9 * NCH;
-            constexpr int PF = NCB == 1 ? 12 : (NCB == 2 ? 8 : 6);
-            uint4 abuf[NSTEP];
-            uint4 bbuf[NSTEP][NCB];
-            auto issue = [&](int st) {
-                const int t = st / NCH, c = st % NCH;
-                abuf[st] = *reinterpret_cast<const uint4*>(dbase + (size_t)max(rows[t], 0) * ROWB_IN + c * 64);
-                const uint4* wp = wbase + ((size_t)t * NCH + c) * NCBT * 64;
+        static_assert(9 * NCH / KS <= 72, "wider contractions take the wide-layer kernel");
+        // narrow inputs: this wavefront's (tap, chunk) steps st = ks + KS*i
+        // are fully unrolled and both operands are prefetched PF steps
+        // ahead, so the weight and delta loads of later taps overlap the
+        // current MFMAs.  The loads are unconditional (clamped step, zero
+        // operand past the end): a load under a branch would make the
+        // compiler drain every outstanding load where the branch joins.
+        constexpr int NSTEP = 9 * NCH;
+        constexpr int NSW = (NSTEP + KS - 1) / KS;
+        constexpr int PF = NCB == 1 ? 12 : (NCB == 2 ? 8 : 6);
+        int srow[NSW];
+        bool sany[NSW];
 #pragma unroll
-                for (int cb = 0; cb < NCB; ++cb) bbuf[st][cb] = wp[cb * 64];
-            };
+        for (int i = 0; i < NSW; ++i) {
+            if constexpr (KS == 1) {
+                srow[i] = rows[i / NCH];
+                sany[i] = any[i / NCH];
+            } else {
+                const int st = ks + KS * i, t = st / NCH;
+                int r = -1;
+                bool an = false;
 #pragma unroll
-            for (int st = 0; st < PF && st < NSTEP; ++st) issue(st);
-#pragma unroll
-            for (int st = 0; st < NSTEP; ++st) {
-                if (st + PF < NSTEP) issue(st + PF);
-                const int t = st / NCH;
-                uint4 av = abuf[st];
-                if (rows[t] < 0) av = make_uint4(0u, 0u, 0u, 0u);
-                if (any[t]) mfma_chunk(av, bbuf[st]);
-                // keep the scheduler from hoisting later loads past this step
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        } else {
-            // wide inputs: one tap at a time, chunks streamed; latency is hidden
-            // by the many resident wavefronts of these larger layers
-            for (int t = 0; t < 9; ++t) {
-                if (!any[t]) continue;
-                const char* arow = dbase + (size_t)max(rows[t], 0) * ROWB_IN;
-                const uint4* wp = wbase + (size_t)t * NCH * NCBT * 64;
-#pragma unroll 4
-                for (int c = 0; c < NCH; ++c) {
-                    uint4 av = *reinterpret_cast<const uint4*>(arow + c * 64);
-                    if (rows[t] < 0) av = make_uint4(0u, 0u, 0u, 0u);
-                    uint4 bv[NCB];
-#pragma unroll
-                    for (int cb = 0; cb < NCB; ++cb) bv[cb] = wp[((size_t)c * NCBT + cb) * 64];
-                    mfma_chunk(av, bv);
+                for (int tt = 0; tt < 9; ++tt) {
+                    r = t == tt ? rows[tt] : r;
+                    an = t == tt ? any[tt] : an;
                 }
+                srow[i] = st < NSTEP ? r : -1;
+                sany[i] = st < NSTEP && an;
             }
         }
+        uint4 abuf[NSW];
+        uint4 bbuf[NSW][NCB];
+        auto issue = [&](int i) {
+            const int st = KS == 1 ? i : min(ks + KS * i, NSTEP - 1);
+            const int c = st % NCH;
+            abuf[i] = *reinterpret_cast<const uint4*>(dbase + (size_t)max(srow[i], 0) * ROWB_IN + c * 64);
+            const uint4* wp = wbase + (size_t)st * NCBT * 64;
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) bbuf[i][cb] = wp[cb * 64];
+        };
+#pragma unroll
+        for (int i = 0; i < PF && i < NSW; ++i) issue(i);
+#pragma unroll
+        for (int i = 0; i < NSW; ++i) {
+            if (i + PF < NSW) issue(i + PF);
+            uint4 av = abuf[i];
+            if (srow[i] < 0) av = make_uint4(0u, 0u, 0u, 0u);
+            if (sany[i]) mfma_chunk(av, bbuf[i]);
+            // keep the scheduler from hoisting later loads past this step
+            __builtin_amdgcn_sched_barrier(0);
+        }
 
-        if (vrow) {
+        if constexpr (KS > 1) {
+            // partial sums of the contraction shares 1..KS-1 into share 0
+            __shared__ f4v red[KS - 1][NWC * NCB][64];
+            if (ks > 0) {
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) red[ks - 1][cw * NCB + cb][lane] = acc[cb];
+            }
+            __syncthreads();
+            if (ks == 0) {
+#pragma unroll
+                for (int j = 0; j < KS - 1; ++j)
+#pragma unroll
+                    for (int cb = 0; cb < NCB; ++cb) {
+                        const f4v p = red[j][cw * NCB + cb][lane];
+                        acc[cb].x += p.x;
+                        acc[cb].y += p.y;
+                        acc[cb].z += p.z;
+                        acc[cb].w += p.w;
+                    }
+            }
+            __syncthreads();                     // read before the next tile writes
+        }
+        if (vrow && ks == 0) {
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
-                const int co0 = (wave * NCB + cb) * 16 + 4 * g;
+                const int co0 = (cw * NCB + cb) * 16 + 4 * g;
                 if (COUT % 16 == 0 || co0 < COUT) epilogue4<COUT, BF16>(a, q, co0, zo[cb], acc[cb]);
             }
         }
@@ -413,7 +449,11 @@ bool layer_supported(int cin, int cout, int stride, bool /*bf16*/) {
 
 template <int CI, int CO, int S, bool BF16>
 static hipError_t launch_shape(const LayerArgs& a, int grid, const LaunchCtx& c) {
-    if constexpr (WideShape<CI, CO, BF16>::NCH > 4 && CO >= 32) {
+    // wide layers: more than 8 input chunks, or more than 4 with at least 8
+    // output blocks (a narrow workgroup would then run 2+ blocks x 72 steps
+    // per wavefront, on half as many workgroups)
+    constexpr int WNCH = WideShape<CI, CO, BF16>::NCH;
+    if constexpr ((WNCH > 8 && CO >= 32) || (WNCH > 4 && CO >= 128)) {
         // tile pairs x cout groups x segments; at most ceil(cap / 32) pairs per segment
         constexpr int NH = WideShape<CI, CO, BF16>::NH;
         int gl = std::max(1, grid / (2 * NH * NSHARD));
