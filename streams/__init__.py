@@ -39,7 +39,8 @@ WEIGHT_SEED = 8557
 __all__ = [
     "LayerSpec", "Workload", "workload", "WORKLOADS", "weights", "make_stream", "UpSpec", "neck", "neck_weights",
     "Stream", "Stride", "round_to_bf16_bits", "bf16_bits_to_f32", "out_shape",
-    "cell_azimuth_sector", "SWEEP_CIN", "SWEEP_COUT",
+    "cell_azimuth_sector", "SWEEP_CIN", "SWEEP_COUT", "PfnSpec", "pfn_spec", "pfn_weights",
+    "make_point_stream",
 ]
 
 
@@ -106,12 +107,50 @@ WORKLOADS = {
     "c5": Workload("c5", 1024, 1024, 64, "f32", tuple(_block(64, 64, 4)), 100, 48000,
                    "1024x1024 drone grid, block 1, 4 concurrent streams"),
     **_sweep_workloads(),
+    "p2": Workload("p2", 504, 504, 64, "f32", tuple(_block(64, 64, 4)), 100, 254016,
+                   "points of the 504x504 drone scan -> incremental pillar feature net (9 -> 64) -> "
+                   "PointPillars block 1"),
 }
 
 
+@dataclasses.dataclass(frozen=True)
+class PfnSpec:
+    """Pillar feature net front end (Sec. III-B): the grid corner in metres,
+    the pillar edge, N points per pillar at most, the window in strides, and a
+    bound on the points of one stride."""
+    x_min: float
+    y_min: float
+    res: float
+    max_points: int
+    window: int
+    max_new_points: int
+
+
+# 504 x 504 pillars of 0.16 m centred on the sensor; N = 100 (Sec. III-B);
+# 100 ms windows of 10 ms strides; every beam of a stride may return.
+PFNS = {"p2": PfnSpec(-40.32, -40.32, 0.16, 100, 10, 2400)}
+
+
+def pfn_spec(name: str) -> PfnSpec:
+    return PFNS[name]
+
+
+def pfn_weights(name: str) -> np.ndarray:
+    """[C0, 9] float32 weights of the pillar feature net's linear layer,
+    He-normal N(0, 2/9); batch norm folded to the identity, no bias."""
+    wl = workload(name)
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence((WEIGHT_SEED, 7, 1000))))
+    return (rng.standard_normal((wl.C0, 9)) * math.sqrt(2.0 / 9.0)).astype(np.float32)
+
+
 def _family(name: str) -> int:
-    """Seed family of a workload: c1..c5 -> 1..5, the single-layer sweep -> 6."""
-    return 6 if name.startswith("l") else int(name[1])
+    """Seed family of a workload: c1..c5 -> 1..5, the single-layer sweep -> 6,
+    the point-level workloads (pillar feature net in front) -> 7."""
+    if name.startswith("l"):
+        return 6
+    if name.startswith("p"):
+        return 7
+    return int(name[1])
 
 
 def workload(name: str) -> Workload:
@@ -262,8 +301,9 @@ _SCAN_RETURN = 0.12             # mean return probability of a beam that reaches
 _SCAN_RETURN_SWING = 0.4        # +-40 % over a 40-stride period (surfaces come and go)
 
 
-def _rosette_hits(rng: np.random.Generator, s: int, H: int, W: int, res: float) -> np.ndarray:
-    """Unique cells hit by the returns of 10 ms stride s (s may be negative)."""
+def _rosette_returns(rng: np.random.Generator, s: int):
+    """Ground hits (x, y) in metres, sensor-grid frame, of the beams of 10 ms
+    stride s that return (s may be negative)."""
     T = 0.01
     t = s * T + np.arange(_SCAN_BEAMS) * (T / _SCAN_BEAMS)
     d = math.radians(_SCAN_PRISM_DEG)
@@ -275,7 +315,34 @@ def _rosette_hits(rng: np.random.Generator, s: int, H: int, W: int, res: float) 
     rng_m = _SCAN_ALT_M / np.tan(-el[keep])               # ground range
     x = rng_m * np.cos(az[keep]) + _SCAN_X0 + _SCAN_SPEED * t[keep]
     y = rng_m * np.sin(az[keep])
+    return x, y
+
+
+def _rosette_hits(rng: np.random.Generator, s: int, H: int, W: int, res: float) -> np.ndarray:
+    """Unique cells hit by the returns of 10 ms stride s (s may be negative)."""
+    x, y = _rosette_returns(rng, s)
     return _metres_to_cells(x, y, H, W, res)
+
+
+def make_point_stream(name: str, seed: int = SCENE_SEED, n_strides: Optional[int] = None) -> List[np.ndarray]:
+    """Point batches of the drone scan for strides -(window-1)..n: float32
+    [n_points, 4] = (x, y, z, intensity), metres in the grid frame.  The first
+    window-1 batches and batch 0 build the first full window (the
+    initialisation of Alg. 1); batches 1..n are the delta strides.  The ground
+    hits are those of the sweep stream's scan; z is ground roughness N(0, 5 cm)
+    and the intensity U(0, 1)."""
+    wl = workload(name)
+    spec = pfn_spec(name)
+    n = wl.n_strides if n_strides is None else n_strides
+    scan = np.random.Generator(np.random.PCG64(np.random.SeedSequence((seed, 6, 0))))
+    attr = np.random.Generator(np.random.PCG64(np.random.SeedSequence((seed, 7, 0))))
+    out = []
+    for s in range(-(spec.window - 1), n + 1):
+        x, y = _rosette_returns(scan, s)
+        z = 0.05 * attr.standard_normal(x.size)
+        r = attr.random(x.size)
+        out.append(np.ascontiguousarray(np.stack([x, y, z, r], axis=1).astype(np.float32)))
+    return out
 
 
 def _thin(cells: np.ndarray, target: int, rng: np.random.Generator) -> np.ndarray:

@@ -86,3 +86,24 @@ def test_sweep_streams_share_cells_and_differ_in_width():
     w = S.weights("l32x8")
     assert len(w) == 1 and w[0].shape == (8, 32, 3, 3)
     assert not np.array_equal(S.weights("l32x16")[0][:8], w[0])
+
+
+def test_point_stream_bins_to_the_paper_sparsity():
+    """Points of the drone scan binned into 0.16 m pillars: ~1,800 occupied and
+    ~480 event-changed pillars per 10 ms stride over 100 ms windows, far below
+    N = 100 points per pillar; the stream is deterministic."""
+    from oracle import pfn as P
+    sp, wl = S.pfn_spec("p2"), S.workload("p2")
+    b = S.make_point_stream("p2", n_strides=40)
+    assert len(b) == 40 + sp.window
+    again = S.make_point_stream("p2", n_strides=40)
+    for x, y in zip(b, again):
+        np.testing.assert_array_equal(x, y)
+        assert x.dtype == np.float32 and x.shape[1] == 4 and len(x) <= sp.max_new_points
+    act, chg = [], []
+    for k in range(sp.window, len(b)):
+        occ, cnt = P.occupancy(b[k - sp.window + 1:k + 1], wl.H, wl.W, sp.x_min, sp.y_min, sp.res)
+        act.append(len(occ))
+        assert cnt.max() < sp.max_points
+        chg.append(len(P.changed_cells(b[k], b[k - sp.window], wl.H, wl.W, sp.x_min, sp.y_min, sp.res)))
+    assert 1400 < np.mean(act) < 2200 and 380 < np.mean(chg) < 600
