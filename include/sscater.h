@@ -42,8 +42,9 @@
  * may run concurrently on different streams.
  *
  * Errors: every call returns 0 or a negative SSCATER_E_* code, never throws.
- * Device-side input faults (a cell index outside the grid or a duplicate
- * index within one stride) set a sticky flag reported as SSCATER_E_DEVICE by
+ * Device-side input faults (a cell index outside the grid, a duplicate
+ * index within one stride, or in points mode a pillar over its point
+ * capacity) set a sticky flag reported as SSCATER_E_DEVICE by
  * the next call that finds it set after the offending stride has executed;
  * sscater_reset clears it.
  */
@@ -111,10 +112,38 @@ typedef struct {
     int32_t count;
 } sscater_pillars;
 
+/* Points mode: the incremental pillar feature net in front of the layers
+ * (Sec. III-B; Alg. 1, PFN part).  The handle keeps, per grid cell (pillar),
+ * a queue of the points of the last `window` strides:
+ *   x_min, y_min : metric position of the grid corner; cell (r, c) holds the
+ *                  points with c = floor((x - x_min) * inv_res) and
+ *                  r = floor((y - y_min) * inv_res), inv_res = 1/res rounded to
+ *                  float32 and every operation in float32; points with
+ *                  0 <= those < W (resp. H) are in the grid, all others
+ *                  (NaN included) are ignored;
+ *   res          : pillar edge (same unit as the points), > 0;
+ *   max_points   : N, points a pillar may hold at once (1..128; the paper's
+ *                  100).  More is a device-side input fault (SSCATER_E_DEVICE,
+ *                  no sampling);
+ *   window       : strides a point stays in the window (1..64; 10 strides of
+ *                  10 ms = 100 ms);
+ *   max_new_points : most points one stride may bring (sizes the queues'
+ *                  bookkeeping; a larger stride is refused with
+ *                  SSCATER_E_OVERFLOW).
+ * A pillar's features are max over its points of ReLU(w . d), d the point's
+ * D = 9 decorated values (x, y, z, intensity, x and y offsets from the pillar
+ * centre, x, y and z offsets from the mean of the pillar's points) and w the
+ * caller's [C0][9] weights (batch norm folded in, no bias).  A pillar is
+ * changed when a point enters or leaves it (event based, Alg. 1). */
+typedef struct {
+    float x_min, y_min, res;
+    int32_t max_points, window, max_new_points;
+} sscater_pfn;
+
 /* Counters of the last stride and running totals since create/reset. */
 typedef struct {
     int32_t n_layers;
-    int32_t pillars;                        /* pillar count of the last stride */
+    int32_t pillars;                        /* pillar count of the last stride (points mode: its points) */
     int64_t steps;                          /* strides since create/reset */
     int64_t active[SSCATER_MAX_LAYERS + 1]; /* |A_l| of the last stride, l = 0..L */
     int64_t pairs[SSCATER_MAX_LAYERS + 1];  /* (input cell, output cell) pairs of layer l = 1..L */
@@ -153,6 +182,27 @@ int sscater_create_neck(const sscater_grid* grid, const sscater_layer* layers, i
                         const void* const* weights, const sscater_upsampler* ups, int32_t n_ups,
                         const void* const* up_weights, sscater_t* out);
 
+/* A handle in points mode (see sscater_pfn): layers and weights as for
+ * sscater_create, C0 <= 64, pfn_weights the host [C0][9] fp32 weights of the
+ * pointwise linear layer (copied).  Strides are then given as points with
+ * sscater_step_points; sscater_step is refused.  Layer 0 (sscater_read,
+ * sscater_changed) is the pseudo-image built by the feature net and its
+ * event-based change set.  Errors as sscater_create, plus
+ * SSCATER_E_INVALID_ARG for a bad sscater_pfn or C0 > 64. */
+int sscater_create_pfn(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
+                       const void* const* weights, const sscater_pfn* pfn, const float* pfn_weights,
+                       sscater_t* out);
+
+/* Advance a points-mode handle by one stride (Alg. 1): points is device
+ * float[n_points][4] = (x, y, z, intensity) of the new stride (NULL when
+ * n_points is 0), valid until the stream has executed the step.  The points
+ * of the stride `window` strides back leave their pillars, the new ones are
+ * queued, every pillar that lost or gained a point gets its features
+ * recomputed from its queue, and the layers follow as in sscater_step.  The
+ * first `window` strides after create/reset build the first full window.
+ * SSCATER_E_OVERFLOW when n_points > max_new_points.  Asynchronous. */
+int sscater_step_points(sscater_t h, const float* points, int32_t n_points, void* stream);
+
 /* Advance by one stride (Alg. 1): detect the changed input cells, then for
  * each layer scatter the deltas into the persistent maps (Eq. 2) and build the
  * next layer's change list.  The first step after create/reset is the full
@@ -187,11 +237,12 @@ int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32
  * Synchronises `stream`. */
 int sscater_stats(sscater_t h, sscater_stats_t* out, void* stream);
 
-/* Metrics extension: per-kernel timing of every launch of sscater_step while
- * enabled, with a pair of HIP events that the kernel's own dispatch stamps at
- * its start and end (hipExtLaunchKernel), so the figure is the kernel's
- * execution time without the event packets' cost.  Slots:
- * 0 = input change detection (present pillars), 1 = vanished pillars,
+/* Metrics extension: per-kernel timing of every launch of sscater_step (and
+ * sscater_step_points) while enabled, with a pair of HIP events that the
+ * kernel's own dispatch stamps at its start and end (hipExtLaunchKernel), so
+ * the figure is the kernel's execution time without the event packets' cost.
+ * Slots: 0 = input change detection (present pillars; points mode: the pillar
+ * queue update), 1 = vanished pillars (points mode: the feature net),
  * 1 + l = layer l (l = 1..L), L + 2 + u = upsampler u of the neck, so
  * L + 2 + n_ups slots in all.  Enable it only for runs that measure kernels. */
 int sscater_profile(sscater_t h, int32_t enable);

@@ -20,6 +20,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -90,6 +91,19 @@ struct sscater {
     long long* cum = nullptr;      // running totals, same layout as one set
     int32_t* err_host = nullptr;   // host-visible sticky error word
     int32_t* err_dev = nullptr;
+    // points mode: the incremental pillar feature net in front of the layers
+    bool pfn = false;
+    sscater_pfn pfn_spec{};
+    float inv_res = 0.f;
+    float4* ring = nullptr;        // [cells][N] point queues
+    uint32_t* head = nullptr;      // [cells] points removed
+    uint32_t* tail = nullptr;      // [cells] points inserted
+    uint32_t* scnt = nullptr;      // [window + 1][cells] points per cell of each stride slot
+    int32_t* touched = nullptr;    // [window + 1][max_new_points] cells each stride slot touched
+    int32_t* tcount = nullptr;     // [window + 1][CSTRIDE] their counters
+    uint32_t* ins_stamp = nullptr; // [cells]
+    int32_t* list0 = nullptr;      // A_0 list, NSHARD segments of cells
+    float* pfn_w = nullptr;        // [C0][9]
     uint32_t epoch = 0;
     int last_set = -1;             // counter set of the last stride, -1 after create/reset
     uint32_t last_epoch = 0;       // epoch of the last stride
@@ -197,6 +211,64 @@ PropTarget prop_target(sscater* h, int l /* consuming layer, 1..L */, int set) {
     return t;
 }
 
+// The layers and the neck of one stride, after A_0 and A_1 are built.
+int run_layers(sscater* h, int set, uint32_t epoch, hipStream_t s) {
+    int32_t* cnt = h->set_ptr(set);
+    hipError_t e = hipSuccess;
+    for (int l = 1; l <= h->L; ++l) {
+        LayerState& ls = h->layers[l - 1];
+        LayerArgs a{};
+        a.list = ls.list;
+        a.count = h->cnt_ptr(set, l);
+        a.cap = ls.Hout * ls.Wout;
+        a.stamp_in = l == 1 ? h->stamp0 : h->layers[l - 2].stamp;
+        a.delta_in = l == 1 ? h->delta0 : h->layers[l - 2].delta;
+        a.wpack = ls.wpack;
+        a.Z = ls.Z;
+        a.delta_out = ls.delta;   // allocated when a later layer or an upsampler reads it
+        a.Hin = ls.Hin;
+        a.Win = ls.Win;
+        a.Hout = ls.Hout;
+        a.Wout = ls.Wout;
+        a.relu = ls.spec.relu;
+        a.epoch = epoch;
+        a.has_next = l < h->L;
+        if (a.has_next) a.next = prop_target(h, l + 1, set);
+        if (l == h->L) {
+            a.cum_src = cnt;
+            a.cum_dst = h->cum;
+            a.n_cum = h->ncnt();
+        }
+        e = timed_launch(h, 1 + l, s, [&](const LaunchCtx& c) {
+            return launch_layer(a, ls.spec.cin, ls.spec.cout, ls.spec.stride, h->bf16, h->layer_grid, c);
+        });
+        if (e != hipSuccess) return hip_fail(e);
+    }
+
+    // the neck: every upsampler over its source layer's change list
+    for (int u = 0; u < h->n_ups; ++u) {
+        const UpState& us = h->ups[u];
+        const LayerState& src = h->layers[us.spec.src_layer - 1];
+        UpArgs a{};
+        a.list = src.list;
+        a.count = h->cnt_ptr(set, us.spec.src_layer);
+        a.cap = src.Hout * src.Wout;
+        a.delta_src = src.delta;
+        a.wpack = us.wpack;
+        a.Z = h->Zn;
+        a.ctot = h->Cn;
+        a.coff = us.coff;
+        a.stamp = h->stamp_n;
+        a.Wsrc = us.Ws;
+        a.epoch = epoch;
+        e = timed_launch(h, h->L + 2 + u, s, [&](const LaunchCtx& c) {
+            return launch_upsample(a, us.cin, us.spec.cout, us.spec.stride, h->bf16, h->layer_grid, c);
+        });
+        if (e != hipSuccess) return hip_fail(e);
+    }
+    return SSCATER_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -208,7 +280,9 @@ const char* sscater_strerror(int code) {
         case SSCATER_E_OUT_OF_MEMORY: return "out of memory";
         case SSCATER_E_HIP: return g_hip_err;
         case SSCATER_E_OVERFLOW: return "pillar count exceeds max_pillars (no sampling)";
-        case SSCATER_E_DEVICE: return "device-side input fault (cell index out of range or duplicate)";
+        case SSCATER_E_DEVICE:
+            return "device-side input fault (cell index out of range, duplicate cell, or a pillar over its point "
+                   "capacity)";
         default: return "unknown error";
     }
 }
@@ -369,7 +443,7 @@ fail:
 }
 
 int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
-    if (!h || !pl) return SSCATER_E_INVALID_ARG;
+    if (!h || !pl || h->pfn) return SSCATER_E_INVALID_ARG;
     if (int rc = check_sticky(h)) return rc;
     const long long cells = (long long)h->grid.H * h->grid.W;
     // NULL idx with count == H*W is dense mode; NULL idx with count 0 is an empty stride
@@ -426,57 +500,7 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
         if (e != hipSuccess) return hip_fail(e);
     }
 
-    for (int l = 1; l <= h->L; ++l) {
-        LayerState& ls = h->layers[l - 1];
-        LayerArgs a{};
-        a.list = ls.list;
-        a.count = h->cnt_ptr(set, l);
-        a.cap = ls.Hout * ls.Wout;
-        a.stamp_in = l == 1 ? h->stamp0 : h->layers[l - 2].stamp;
-        a.delta_in = l == 1 ? h->delta0 : h->layers[l - 2].delta;
-        a.wpack = ls.wpack;
-        a.Z = ls.Z;
-        a.delta_out = ls.delta;   // allocated when a later layer or an upsampler reads it
-        a.Hin = ls.Hin;
-        a.Win = ls.Win;
-        a.Hout = ls.Hout;
-        a.Wout = ls.Wout;
-        a.relu = ls.spec.relu;
-        a.epoch = epoch;
-        a.has_next = l < h->L;
-        if (a.has_next) a.next = prop_target(h, l + 1, set);
-        if (l == h->L) {
-            a.cum_src = cnt;
-            a.cum_dst = h->cum;
-            a.n_cum = h->ncnt();
-        }
-        e = timed_launch(h, 1 + l, s, [&](const LaunchCtx& c) {
-            return launch_layer(a, ls.spec.cin, ls.spec.cout, ls.spec.stride, h->bf16, h->layer_grid, c);
-        });
-        if (e != hipSuccess) return hip_fail(e);
-    }
-
-    // the neck: every upsampler over its source layer's change list
-    for (int u = 0; u < h->n_ups; ++u) {
-        const UpState& us = h->ups[u];
-        const LayerState& src = h->layers[us.spec.src_layer - 1];
-        UpArgs a{};
-        a.list = src.list;
-        a.count = h->cnt_ptr(set, us.spec.src_layer);
-        a.cap = src.Hout * src.Wout;
-        a.delta_src = src.delta;
-        a.wpack = us.wpack;
-        a.Z = h->Zn;
-        a.ctot = h->Cn;
-        a.coff = us.coff;
-        a.stamp = h->stamp_n;
-        a.Wsrc = us.Ws;
-        a.epoch = epoch;
-        e = timed_launch(h, h->L + 2 + u, s, [&](const LaunchCtx& c) {
-            return launch_upsample(a, us.cin, us.spec.cout, us.spec.stride, h->bf16, h->layer_grid, c);
-        });
-        if (e != hipSuccess) return hip_fail(e);
-    }
+    if (int rc = run_layers(h, set, epoch, s)) return rc;
 
     if (!dense) {
         h->prev_slot = cur_slot;
@@ -490,6 +514,136 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
     h->last_epoch = epoch;
     h->steps += 1;
     h->last_pillars = pl->count;
+    return SSCATER_OK;
+}
+
+int sscater_create_pfn(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
+                       const void* const* weights, const sscater_pfn* pfn, const float* pfn_weights,
+                       sscater_t* out) {
+    if (!grid || !pfn || !pfn_weights || !out) return SSCATER_E_INVALID_ARG;
+    *out = nullptr;
+    const sscater_pfn& p = *pfn;
+    if (!(p.res > 0.f) || !std::isfinite(p.res) || !std::isfinite(p.x_min) || !std::isfinite(p.y_min) ||
+        p.max_points < 1 || p.max_points > 128 || p.window < 1 || p.window > 64 || p.max_new_points < 0 ||
+        p.max_new_points > (1 << 24) || grid->C0 < 1 || grid->C0 > 64)
+        return SSCATER_E_INVALID_ARG;
+    sscater_t h = nullptr;
+    int rc = sscater_create_neck(grid, layers, n_layers, weights, nullptr, 0, nullptr, &h);
+    if (rc != SSCATER_OK) return rc;
+    DeviceGuard dg(h->device);
+    if (!dg.ok) {
+        sscater_destroy(h);
+        return hip_fail(hipGetLastError());
+    }
+    const size_t cells = (size_t)grid->H * grid->W;
+    const size_t slots = (size_t)p.window + 1;
+    const size_t per_slot = (size_t)std::max(p.max_new_points, 1);
+    hipError_t he = hipSuccess;
+    h->pfn = true;
+    h->pfn_spec = p;
+    h->inv_res = 1.0f / p.res;
+    if ((rc = dev_alloc(h, (void**)&h->ring, cells * (size_t)p.max_points * sizeof(float4))) != SSCATER_OK ||
+        (rc = dev_alloc(h, (void**)&h->head, cells * 4)) != SSCATER_OK ||
+        (rc = dev_alloc(h, (void**)&h->tail, cells * 4)) != SSCATER_OK ||
+        (rc = dev_alloc(h, (void**)&h->scnt, slots * cells * 4)) != SSCATER_OK ||
+        (rc = dev_alloc(h, (void**)&h->touched, slots * per_slot * 4)) != SSCATER_OK ||
+        (rc = dev_alloc(h, (void**)&h->tcount, slots * CSTRIDE * 4)) != SSCATER_OK ||
+        (rc = dev_alloc(h, (void**)&h->ins_stamp, cells * 4)) != SSCATER_OK ||
+        (rc = dev_alloc(h, (void**)&h->list0, (size_t)NSHARD * cells * 4)) != SSCATER_OK ||
+        (rc = dev_alloc(h, (void**)&h->pfn_w, (size_t)grid->C0 * 9 * 4)) != SSCATER_OK) {
+        sscater_destroy(h);
+        return rc;
+    }
+    he = hipMemcpy(h->pfn_w, pfn_weights, (size_t)grid->C0 * 9 * 4, hipMemcpyHostToDevice);
+    if (he == hipSuccess) he = hipDeviceSynchronize();
+    if (he != hipSuccess) {
+        rc = hip_fail(he);
+        sscater_destroy(h);
+        return rc;
+    }
+    *out = h;
+    return SSCATER_OK;
+}
+
+int sscater_step_points(sscater_t h, const float* points, int32_t n_points, void* stream) {
+    if (!h || !h->pfn || n_points < 0 || (n_points > 0 && !points)) return SSCATER_E_INVALID_ARG;
+    if (n_points > h->pfn_spec.max_new_points) return SSCATER_E_OVERFLOW;
+    if (int rc = check_sticky(h)) return rc;
+    DeviceGuard dg(h->device);
+    if (!dg.ok) return hip_fail(hipGetLastError());
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const sscater_pfn& p = h->pfn_spec;
+    const int cells = h->grid.H * h->grid.W;
+    const uint32_t epoch = ++h->epoch;
+    const int set = (int)(epoch & 1u);
+    // stride slots: this stride inserts into slot steps % (window + 1); the
+    // stride that leaves the window (steps - window) used slot (steps + 1) % (window + 1)
+    const int slots = p.window + 1;
+    const int ins = (int)(h->steps % slots), pop = (int)((h->steps + 1) % slots);
+    const size_t per_slot = (size_t)std::max(p.max_new_points, 1);
+
+    PillarArgs u{};
+    u.points = reinterpret_cast<const float4*>(points);
+    u.n_points = n_points;
+    u.x_min = p.x_min;
+    u.y_min = p.y_min;
+    u.inv_res = h->inv_res;
+    u.H = h->grid.H;
+    u.W = h->grid.W;
+    u.N = p.max_points;
+    u.ring = h->ring;
+    u.head = h->head;
+    u.tail = h->tail;
+    u.scnt_ins = h->scnt + (size_t)ins * cells;
+    u.scnt_pop = h->scnt + (size_t)pop * cells;
+    u.touched_ins = h->touched + (size_t)ins * per_slot;
+    u.tcount_ins = h->tcount + (size_t)ins * CSTRIDE;
+    u.touched_pop = h->touched + (size_t)pop * per_slot;
+    u.tcount_pop = h->tcount + (size_t)pop * CSTRIDE;
+    u.ins_stamp = h->ins_stamp;
+    u.stamp0 = h->stamp0;
+    u.list0 = h->list0;
+    u.count0 = h->cnt_ptr(set, 0);
+    u.zero_ptr = h->set_ptr(set ^ 1);
+    u.zero_n = h->ncnt();
+    u.epoch = epoch;
+    // the leaving stride touched at most max_new_points cells
+    u.n_pop_blocks = std::max(1, std::min(64, (p.max_new_points + 255) / 256));
+    const int ins_blocks = std::max(1, std::min(256, (n_points + 255) / 256));
+    hipError_t e = timed_launch(h, 0, s, [&](const LaunchCtx& c) { return launch_pillar_update(u, ins_blocks, c); });
+    if (e != hipSuccess) return hip_fail(e);
+
+    PfnArgs f{};
+    f.list0 = h->list0;
+    f.count0 = h->cnt_ptr(set, 0);
+    f.cap0 = cells;
+    f.ring = h->ring;
+    f.head = h->head;
+    f.tail = h->tail;
+    f.N = p.max_points;
+    f.w = h->pfn_w;
+    f.C0 = h->grid.C0;
+    f.W = h->grid.W;
+    f.x_min = p.x_min;
+    f.y_min = p.y_min;
+    f.res = p.res;
+    f.X = h->X;
+    f.delta0 = h->delta0;
+    f.tcount_clear = h->tcount + (size_t)pop * CSTRIDE;   // the next stride inserts into this slot
+    f.err = h->err_dev;
+    f.epoch = epoch;
+    f.next = prop_target(h, 1, set);
+    // |A_0| <= the leaving stride's cells + this stride's points; one wavefront per pillar
+    const long long bound = (long long)p.max_new_points + n_points;
+    const int pfn_blocks = (int)std::max(1LL, std::min(1024LL, (bound + 3) / 4));
+    e = timed_launch(h, 1, s, [&](const LaunchCtx& c) { return launch_pfn(f, h->bf16, pfn_blocks, c); });
+    if (e != hipSuccess) return hip_fail(e);
+
+    if (int rc = run_layers(h, set, epoch, s)) return rc;
+    h->last_set = set;
+    h->last_epoch = epoch;
+    h->steps += 1;
+    h->last_pillars = n_points;
     return SSCATER_OK;
 }
 
@@ -541,6 +695,13 @@ int sscater_reset(sscater_t h, void* stream) {
     if (e == hipSuccess && h->Zn) e = launch_fill_zero(h->Zn, round_up((size_t)h->Hn * h->Wn * h->Cn * 4, 256), s);
     if (e == hipSuccess) e = launch_fill_zero(h->counters, round_up((size_t)2 * h->ncnt() * 4, 256), s);
     if (e == hipSuccess) e = launch_fill_zero(h->cum, round_up((size_t)h->ncnt() * 8, 256), s);
+    if (e == hipSuccess && h->pfn) {
+        const size_t slots = (size_t)h->pfn_spec.window + 1;
+        e = launch_fill_zero(h->head, round_up(cells * 4, 256), s);
+        if (e == hipSuccess) e = launch_fill_zero(h->tail, round_up(cells * 4, 256), s);
+        if (e == hipSuccess) e = launch_fill_zero(h->scnt, round_up(slots * cells * 4, 256), s);
+        if (e == hipSuccess) e = launch_fill_zero(h->tcount, round_up(slots * CSTRIDE * 4, 256), s);
+    }
     if (e != hipSuccess) return hip_fail(e);
     ++h->epoch;   // every stamp becomes stale
     h->prev_count = 0;

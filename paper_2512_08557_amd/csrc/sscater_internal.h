@@ -93,7 +93,59 @@ struct UpArgs {
     uint32_t epoch;
 };
 
-enum ErrBits { ERR_INDEX_RANGE = 1, ERR_DUPLICATE = 2 };
+// Pillar point queues of the incremental pillar feature net: every cell holds
+// a ring of N points; tail counts the points ever inserted, head those
+// removed, so the live points are ring positions head..tail-1 (mod N).  The
+// points of one stride leave the window together, `window` strides later, so
+// per-stride slots (window + 1 of them) keep, per cell, how many points that
+// stride inserted and the list of cells it touched.
+struct PillarArgs {
+    const float4* points;       // this stride's points (x, y, z, intensity)
+    int n_points;
+    float x_min, y_min, inv_res;
+    int H, W, N;
+    float4* ring;               // [H*W][N]
+    uint32_t* head;             // [H*W]
+    uint32_t* tail;             // [H*W]
+    uint32_t* scnt_ins;         // [H*W] points per cell of this stride's slot
+    uint32_t* scnt_pop;         // [H*W] ... of the slot of the stride leaving the window
+    int32_t* touched_ins;       // cells first touched by this stride, and their counter
+    int32_t* tcount_ins;
+    const int32_t* touched_pop; // cells the leaving stride touched, and their count
+    const int32_t* tcount_pop;
+    uint32_t* ins_stamp;        // [H*W] epoch of a cell's last insertion
+    uint32_t* stamp0;           // [H*W] A_0 stamps
+    int32_t* list0;             // A_0 list, NSHARD segments of H*W
+    int32_t* count0;            // its counters, segment k at [k * CSTRIDE]
+    int32_t* zero_ptr;          // counter set of the next stride, cleared here
+    int zero_n;
+    uint32_t epoch;
+    int n_pop_blocks;           // workgroups [0, n_pop_blocks) remove, the others insert
+};
+
+// The pillar feature net over A_0: decoration, pointwise linear layer, ReLU
+// and max over each changed pillar's points; the canvas update, the input
+// deltas and A_0 -> A_1 propagation as in change detection.
+struct PfnArgs {
+    const int32_t* list0;
+    const int32_t* count0;
+    int cap0;                   // cells per list segment
+    const float4* ring;
+    const uint32_t* head;
+    const uint32_t* tail;
+    int N;
+    const float* w;             // [C0][9]
+    int C0, W;
+    float x_min, y_min, res;
+    void* X;                    // canvas [H*W][C0] (grid dtype)
+    void* delta0;               // input deltas dense by cell
+    int32_t* tcount_clear;      // counter of the next stride's insertion slot, cleared here
+    int32_t* err;
+    uint32_t epoch;
+    PropTarget next;
+};
+
+enum ErrBits { ERR_INDEX_RANGE = 1, ERR_DUPLICATE = 2, ERR_PILLAR_FULL = 4 };
 
 // Where a launch goes: its stream and, while kernel timing is on, two events
 // that the dispatch packet itself stamps when the kernel starts and ends
@@ -129,6 +181,8 @@ size_t up_wpack_elems(int cin, int cout, int stride, bool bf16);
 // into the layout the upsampling kernel reads.
 void pack_up_weights(const void* w, int cin, int cout, int stride, bool bf16, void* dst);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_pillar_update(const PillarArgs& a, int insert_blocks, const LaunchCtx& c);
+hipError_t launch_pfn(const PfnArgs& a, bool bf16, int blocks, const LaunchCtx& c);
 size_t wpack_elems(int cin, int cout, bool bf16);
 // Repack OIHW weights (fp32 values, or bf16 bit patterns) into the layout the
 // layer kernel reads; dst holds wpack_elems() elements of 4 (fp32) or 2 (bf16) bytes.

@@ -23,9 +23,9 @@ OK, E_INVALID_ARG, E_OUT_OF_MEMORY, E_HIP, E_OVERFLOW, E_DEVICE = 0, -1, -2, -3,
 F32, BF16 = 0, 1
 
 # every function declared in include/sscater.h
-EXPORTS = ("sscater_create", "sscater_create_neck", "sscater_step", "sscater_read", "sscater_reset",
-           "sscater_destroy", "sscater_changed", "sscater_stats", "sscater_profile", "sscater_profile_read",
-           "sscater_strerror")
+EXPORTS = ("sscater_create", "sscater_create_neck", "sscater_create_pfn", "sscater_step", "sscater_step_points",
+           "sscater_read", "sscater_reset", "sscater_destroy", "sscater_changed", "sscater_stats", "sscater_profile",
+           "sscater_profile_read", "sscater_strerror")
 
 
 class Grid(ctypes.Structure):
@@ -41,6 +41,11 @@ class Layer(ctypes.Structure):
 class Upsampler(ctypes.Structure):
     _fields_ = [("src_layer", ctypes.c_int32), ("cout", ctypes.c_int32), ("stride", ctypes.c_int32),
                 ("relu", ctypes.c_int32)]
+
+
+class Pfn(ctypes.Structure):
+    _fields_ = [("x_min", ctypes.c_float), ("y_min", ctypes.c_float), ("res", ctypes.c_float),
+                ("max_points", ctypes.c_int32), ("window", ctypes.c_int32), ("max_new_points", ctypes.c_int32)]
 
 
 class Pillars(ctypes.Structure):
@@ -77,7 +82,11 @@ def lib() -> ctypes.CDLL:
         L.sscater_create_neck.argtypes = [ctypes.POINTER(Grid), ctypes.POINTER(Layer), i32,
                                           ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(Upsampler), i32,
                                           ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(vp)]
+        L.sscater_create_pfn.argtypes = [ctypes.POINTER(Grid), ctypes.POINTER(Layer), i32,
+                                         ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(Pfn),
+                                         ctypes.POINTER(ctypes.c_float), ctypes.POINTER(vp)]
         L.sscater_step.argtypes = [vp, ctypes.POINTER(Pillars), vp]
+        L.sscater_step_points.argtypes = [vp, vp, i32, vp]
         L.sscater_read.argtypes = [vp, i32, vp, ctypes.c_size_t, vp]
         L.sscater_reset.argtypes = [vp, vp]
         L.sscater_destroy.argtypes = [vp]
@@ -120,10 +129,14 @@ class Engine:
 
     def __init__(self, H: int, W: int, C0: int, layers: Sequence[Tuple[int, int, int, bool]],
                  weights: Sequence[np.ndarray], dtype: str = "f32", max_pillars: int = 16000,
-                 ups: Sequence[Tuple[int, int, int, bool]] = (), up_weights: Sequence[np.ndarray] = ()):
+                 ups: Sequence[Tuple[int, int, int, bool]] = (), up_weights: Sequence[np.ndarray] = (),
+                 pfn=None, pfn_weights: Optional[np.ndarray] = None):
         """layers: (cin, cout, stride, relu); weights: OIHW per layer.  ups:
         optional neck, (src_layer, cout, stride, relu) per upsampler with
-        [cin, cout, s, s] weights; the neck map is layer len(layers) + 1."""
+        [cin, cout, s, s] weights; the neck map is layer len(layers) + 1.
+        pfn: optional points mode, (x_min, y_min, res, max_points, window,
+        max_new_points) with [C0, 9] float32 pfn_weights; strides are then
+        given to step_points."""
         import torch  # device memory and streams only
         self._torch = torch
         self.H, self.W, self.C0 = H, W, C0
@@ -143,7 +156,19 @@ class Engine:
         wptrs = (ctypes.c_void_p * n)(*[b.ctypes.data for b in self._wbufs])
         handle = ctypes.c_void_p()
         self.ups = [tuple(u) for u in ups]
-        if self.ups:
+        self.pfn = tuple(pfn) if pfn is not None else None
+        if self.pfn is not None:
+            if self.ups:
+                raise ValueError("points mode takes no neck")
+            pw = np.ascontiguousarray(pfn_weights, dtype=np.float32)
+            if pw.shape != (C0, 9):
+                raise ValueError("pfn_weights must be [C0, 9]")
+            spec = Pfn(float(self.pfn[0]), float(self.pfn[1]), float(self.pfn[2]), int(self.pfn[3]),
+                       int(self.pfn[4]), int(self.pfn[5]))
+            _check(lib().sscater_create_pfn(ctypes.byref(grid), larr, n, wptrs, ctypes.byref(spec),
+                                            pw.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                                            ctypes.byref(handle)), "sscater_create_pfn")
+        elif self.ups:
             nu = len(self.ups)
             if len(up_weights) != nu:
                 raise ValueError("one weight tensor per upsampler")
@@ -187,6 +212,18 @@ class Engine:
             raise ValueError("feats must be a contiguous cuda tensor [count, C0] of the grid dtype")
         p = Pillars(idx.data_ptr() if idx is not None else None, feats.data_ptr() if count else None, count)
         _check(lib().sscater_step(self._h, ctypes.byref(p), self._stream(stream)), "sscater_step")
+
+    def step_points(self, points, stream=None) -> None:
+        """points: contiguous float32 cuda tensor [n, 4] = (x, y, z, intensity)
+        of one stride (points mode)."""
+        n = 0
+        if points is not None:
+            if points.dtype != self._torch.float32 or not points.is_cuda or not points.is_contiguous() or \
+                    points.dim() != 2 or points.shape[1] != 4:
+                raise ValueError("points must be a contiguous float32 cuda tensor [n, 4]")
+            n = points.shape[0]
+        ptr = ctypes.c_void_p(points.data_ptr() if n else None)
+        _check(lib().sscater_step_points(self._h, ptr, n, self._stream(stream)), "sscater_step_points")
 
     def read(self, layer: int, out=None, stream=None):
         h, w, c = self.shapes[layer]

@@ -58,8 +58,15 @@ def map_errors(eng, ys_ref):
     return out
 
 
-def check_maps(eng, ys_ref, tol, where=""):
+def check_maps(eng, ys_ref, tol, where="", floors=None):
+    """max|gpu - ref| <= tol * max|ref| per layer.  floors: optional per-layer
+    scale to use instead when it is larger (the largest max|ref| the layer held
+    earlier in the run: once a window drains to zero, recycled maps keep the
+    rounding residue of the deltas that cancelled, which only that earlier
+    scale measures)."""
     for l, (err, scale) in enumerate(map_errors(eng, ys_ref), start=1):
+        if floors is not None:
+            scale = max(scale, floors[l - 1])
         if scale == 0.0:
             assert err <= 1e-6, f"{where} layer {l}: reference is zero, max|gpu| = {err}"
         else:

@@ -146,3 +146,59 @@ def test_create_neck_rejects_invalid_arguments(case):
     elif case == "too_many":
         ups = ups * 3
     assert _create_neck(g, L, ups, up_w) == ssc.E_INVALID_ARG
+
+
+def _create_pfn(grid, layers, pfn, pfn_w=True):
+    lib = ssc.lib()
+    n = len(layers)
+    larr = (E.Layer * n)(*layers)
+    bufs = [np.zeros((l.cout, l.cin, 3, 3), np.float32) for l in layers]
+    wp = (ctypes.c_void_p * n)(*[b.ctypes.data for b in bufs])
+    pw = np.zeros((max(grid.C0, 1), 9), np.float32)
+    ptr = pw.ctypes.data_as(ctypes.POINTER(ctypes.c_float)) if pfn_w else None
+    h = ctypes.c_void_p()
+    rc = lib.sscater_create_pfn(ctypes.byref(grid), larr, n, wp, ctypes.byref(pfn) if pfn is not None else None,
+                                ptr, ctypes.byref(h))
+    if rc == ssc.OK:
+        lib.sscater_destroy(h)
+    return rc
+
+
+@pytest.mark.parametrize("case", ["no_spec", "no_weights", "res0", "res_nan", "corner_inf", "points0",
+                                  "points129", "window0", "window65", "new_neg", "c0_wide", "bad_layers"])
+def test_create_pfn_rejects_invalid_arguments(case):
+    """Every check runs on the host before any HIP call."""
+    g = E.Grid(16, 16, 64, 0, E.F32)
+    L = [E.Layer(64, 64, 3, 1, 1, 1)]
+    p = E.Pfn(-1.28, -1.28, 0.16, 100, 10, 2400)
+    w = True
+    if case == "no_spec":
+        p = None
+    elif case == "no_weights":
+        w = False
+    elif case == "res0":
+        p.res = 0.0
+    elif case == "res_nan":
+        p.res = float("nan")
+    elif case == "corner_inf":
+        p.x_min = float("inf")
+    elif case == "points0":
+        p.max_points = 0
+    elif case == "points129":
+        p.max_points = 129
+    elif case == "window0":
+        p.window = 0
+    elif case == "window65":
+        p.window = 65
+    elif case == "new_neg":
+        p.max_new_points = -1
+    elif case == "c0_wide":
+        g = E.Grid(16, 16, 128, 0, E.F32)
+        L = [E.Layer(128, 64, 3, 1, 1, 1)]
+    elif case == "bad_layers":
+        L = [E.Layer(32, 64, 3, 1, 1, 1)]
+    assert _create_pfn(g, L, p, w) == ssc.E_INVALID_ARG
+
+
+def test_points_calls_reject_null_handle():
+    assert ssc.lib().sscater_step_points(None, None, 0, None) == ssc.E_INVALID_ARG
