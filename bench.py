@@ -69,11 +69,11 @@ def upload(strides, dtype):
     return out
 
 
-def kernel_name(slot: int, wl, ups=()) -> str:
+def kernel_name(slot: int, wl, ups=(), points=False) -> str:
     if slot == 0:
-        return "detect_kernel<present>"
+        return "pillar_update_kernel" if points else "detect_kernel<present>"
     if slot == 1:
-        return "detect_kernel<vanished>"
+        return f"pfn_kernel<{wl.dtype}>" if points else "detect_kernel<vanished>"
     if slot >= len(wl.layers) + 2:
         u = ups[slot - len(wl.layers) - 2]
         cin = wl.layers[u.src - 1].cout
@@ -112,6 +112,37 @@ def cpu_baseline(wl, ws, strides, first, budget_s, neck=()):
                       f"all {len(layers)} layers{' and the neck' if ups else ''} plus the per-layer change lists "
                       f"({t_total:.1f} s, "
                       f"{t_total / n * 1e3:.1f} ms per stride)"}
+
+
+def cpu_baseline_points(wl, ws, spec, pw, batches, first, budget_s):
+    """Points mode: the oracle's pillar feature net over each window, the dense
+    float64 recompute of every layer and the event-based change lists, on
+    consecutive strides of the timed range until the time budget is spent."""
+    import oracle
+    from oracle import pfn as P
+    layers = layers_of(wl)
+    t_total, u_total, n = 0.0, 0, 0
+    for k in range(first, len(batches)):
+        t0 = time.perf_counter()
+        x = P.canvas(batches[k - spec.window + 1:k + 1], wl.H, wl.W, spec.x_min, spec.y_min, spec.res, pw)
+        oracle.forward(x, ws, layers)
+        a0 = P.changed_cells(batches[k], batches[k - spec.window], wl.H, wl.W, spec.x_min, spec.y_min, spec.res)
+        m = np.zeros(wl.H * wl.W, dtype=bool)
+        m[a0] = True
+        m = m.reshape(wl.H, wl.W)
+        act = [len(a0)]
+        for l in wl.layers[:-1]:
+            m = oracle.propagate_gather(m, l.stride)
+            act.append(int(m.sum()))
+        t_total += time.perf_counter() - t0
+        u_total += sum(act)
+        n += 1
+        if t_total >= budget_s:
+            break
+    return {"value": u_total / t_total, "unit": "updates/s", "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"{n} consecutive delta strides of the timed range, each the pillar feature net over the "
+                      f"window's points plus a dense float64 recompute of all {len(layers)} layers and the change "
+                      f"lists ({t_total:.1f} s, {t_total / n * 1e3:.1f} ms per stride)"}
 
 
 # --------------------------------------------------------------------------
@@ -386,22 +417,39 @@ def main() -> int:
     ws = S.weights(args.workload)
     K, W = args.steps, args.warmup
     log(f"[bench] workload {wl.name}: {wl.description}; generating {W + K} delta strides")
-    strides = S.make_stream(wl.name, n_strides=W + K)
-    dev = upload(strides, wl.dtype)
     neck = S.neck(wl.name) if args.neck else ()
     if args.neck and not neck:
         log(f"bench.py: workload {wl.name} has no neck")
         return 2
-    eng = Engine(wl.H, wl.W, wl.C0, layers_of(wl), ws, dtype=wl.dtype, max_pillars=wl.max_pillars,
-                 ups=[(u.src, u.cout, u.stride, u.relu) for u in neck], up_weights=S.neck_weights(wl.name) if neck else ())
+    spec = S.PFNS.get(wl.name)
+    if spec is not None:
+        # points mode: batches -(window-1)..0 build the first window
+        strides = S.make_point_stream(wl.name, n_strides=W + K)
+        first = spec.window
+        dev = [torch.from_numpy(b).cuda() for b in strides]
+        torch.cuda.synchronize()
+        pw = S.pfn_weights(wl.name)
+        # sized so that one step may take a whole window's points (the full recompute)
+        eng = Engine(wl.H, wl.W, wl.C0, layers_of(wl), ws, dtype=wl.dtype, max_pillars=0,
+                     pfn=(spec.x_min, spec.y_min, spec.res, spec.max_points, spec.window,
+                          spec.window * spec.max_new_points), pfn_weights=pw)
+        step = lambda k: eng.step_points(dev[k])
+    else:
+        strides = S.make_stream(wl.name, n_strides=W + K)
+        first = 1
+        dev = upload(strides, wl.dtype)
+        eng = Engine(wl.H, wl.W, wl.C0, layers_of(wl), ws, dtype=wl.dtype, max_pillars=wl.max_pillars,
+                     ups=[(u.src, u.cout, u.stride, u.relu) for u in neck],
+                     up_weights=S.neck_weights(wl.name) if neck else ())
+        step = lambda k: eng.step(*dev[k])
     L = len(wl.layers)
 
     def run_range(lo, hi):
         for k in range(lo, hi):
-            eng.step(*dev[k])
+            step(k)
 
     # full window + warmup (untimed)
-    run_range(0, 1 + W)
+    run_range(0, first + W)
     torch.cuda.synchronize()
     before = eng.stats()
 
@@ -409,7 +457,7 @@ def main() -> int:
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    run_range(1 + W, 1 + W + K)
+    run_range(first + W, first + W + K)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     after = eng.stats()
@@ -417,12 +465,12 @@ def main() -> int:
 
     # ---- latency pass: the same strides again, a HIP event after each ----
     eng.reset()
-    run_range(0, 1 + W)
+    run_range(0, first + W)
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
     torch.cuda.synchronize()
     evs[0].record(stream)
     for k in range(K):
-        eng.step(*dev[1 + W + k])
+        step(first + W + k)
         evs[k + 1].record(stream)
     torch.cuda.synchronize()
     per_stride = [evs[k].elapsed_time(evs[k + 1]) for k in range(K)]
@@ -440,11 +488,11 @@ def main() -> int:
     kernels = {}
     if not args.no_profile:
         eng.reset()
-        run_range(0, 1 + W)
+        run_range(0, first + W)
         eng.profile_read()               # drop anything recorded so far
         b2 = eng.stats()
         eng.profile(True)
-        run_range(1 + W, 1 + W + K)
+        run_range(first + W, first + W + K)
         ms, cnt = eng.profile_read()
         eng.profile(False)
         a2 = eng.stats()
@@ -454,7 +502,7 @@ def main() -> int:
         for slot in range(L + 2 + len(neck)):
             if cnt[slot] == 0:
                 continue
-            name = kernel_name(slot, wl, neck)
+            name = kernel_name(slot, wl, neck, points=spec is not None)
             k = kernels.setdefault(name, {"ms": 0.0, "launches": 0, "flops": 0.0, "bytes": 0.0})
             k["ms"] += ms[slot]
             k["launches"] += cnt[slot]
@@ -494,14 +542,18 @@ def main() -> int:
 
     # ---- GPU full recompute: reset + full window through the same kernels ----
     full = []
-    last = dev[W + K]
+    if spec is not None:       # every point of the last window in one step
+        last_pts = torch.cat(dev[first + W + K - spec.window:first + W + K]).contiguous()
+        full_step = lambda: eng.step_points(last_pts)
+    else:
+        full_step = lambda: eng.step(*dev[W + K])
     for _ in range(0 if args.no_full else 5):
         eng.reset()
         torch.cuda.synchronize()
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
         a.record(stream)
-        eng.step(*last)
+        full_step()
         b.record(stream)
         torch.cuda.synchronize()
         full.append(a.elapsed_time(b))
@@ -512,7 +564,10 @@ def main() -> int:
     if not args.no_cpu:
         try:
             log(f"[bench] CPU oracle baseline (budget {args.cpu_seconds:.0f} s)")
-            cpu = cpu_baseline(wl, ws, strides, 1 + W, args.cpu_seconds, neck)
+            if spec is not None:
+                cpu = cpu_baseline_points(wl, ws, spec, pw, strides, first + W, args.cpu_seconds)
+            else:
+                cpu = cpu_baseline(wl, ws, strides, 1 + W, args.cpu_seconds, neck)
         except Exception as exc:  # the oracle is optional for the GPU number
             log(f"[bench] CPU baseline skipped: {exc}")
 
@@ -525,7 +580,10 @@ def main() -> int:
                    "layers": [f"{l.cin}->{l.cout} s{l.stride}{' relu' if l.relu else ''}" for l in wl.layers],
                    "neck": [f"up(layer {u.src}) {wl.layers[u.src - 1].cout}->{u.cout} x{u.stride}" for u in neck],
                    "strides": "full window + warmup untimed, then the timed delta strides",
-                   "mean_pillars": float(np.mean([len(s.idx) for s in strides[1 + W:]])),
+                   **({"mean_points": float(np.mean([len(b) for b in strides[first + W:]])),
+                       "pillar_feature_net": f"9 -> {wl.C0}, N = {spec.max_points}, window {spec.window} strides"}
+                      if spec is not None else
+                      {"mean_pillars": float(np.mean([len(s.idx) for s in strides[1 + W:]]))}),
                    "mean_active": [a / K for a in act_in]},
         # per-stride latency from a second pass with an event after every stride
         "latency_ms": {"mean": statistics.fmean(per_stride), "p50": srt[len(srt) // 2],
