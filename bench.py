@@ -69,6 +69,15 @@ def upload(strides, dtype):
     return out
 
 
+def layer_kernel_name(cin: int, cout: int, stride: int, dtype: str) -> str:
+    """The library's kernel for a layer: the wide-layer kernel takes more than
+    8 input chunks of 16 channels with cout >= 32, or more than 4 with
+    cout >= 128; every other layer the narrow one."""
+    nch = cin // 16
+    wide = (nch > 8 and cout >= 32) or (nch > 4 and cout >= 128)
+    return f"layer_kernel{'_wide' if wide else ''}<{cin},{cout},{stride},{dtype}>"
+
+
 def kernel_name(slot: int, wl, ups=(), points=False) -> str:
     if slot == 0:
         return "pillar_update_kernel" if points else "detect_kernel<present>"
@@ -79,7 +88,7 @@ def kernel_name(slot: int, wl, ups=(), points=False) -> str:
         cin = wl.layers[u.src - 1].cout
         return f"upsample_kernel<{cin},{u.cout},{u.stride},{wl.dtype}>"
     l = wl.layers[slot - 2]
-    return f"layer_kernel<{l.cin},{l.cout},{l.stride},{wl.dtype}>"
+    return layer_kernel_name(l.cin, l.cout, l.stride, wl.dtype)
 
 
 def cpu_baseline(wl, ws, strides, first, budget_s, neck=()):
@@ -193,15 +202,17 @@ def short_kernel(name: str) -> str:
     dt = lambda v: "bf16" if v == "true" else "f32"
     if fn == "detect_kernel" and len(t) == 3:
         return f"detect_kernel<{t[0]},{dt(t[1])},{'vanished' if t[2] == 'true' else 'present'}>"
-    if fn == "layer_kernel" and len(t) == 4:
-        return f"layer_kernel<{t[0]},{t[1]},{t[2]},{dt(t[3])}>"
+    if fn in ("layer_kernel", "layer_kernel_wide") and len(t) == 4:
+        return f"{fn}<{t[0]},{t[1]},{t[2]},{dt(t[3])}>"
+    if fn == "pfn_kernel" and len(t) == 1:
+        return f"pfn_kernel<{dt(t[0])}>"
     return fn + "<" + ",".join(t) + ">"
 
 
 def launches_per_stride(kernel: str, wl) -> int:
-    if kernel.startswith("detect_kernel"):
+    if kernel.startswith(("detect_kernel", "pillar_update_kernel", "pfn_kernel")):
         return 1
-    return sum(1 for l in wl.layers if f"layer_kernel<{l.cin},{l.cout},{l.stride},{wl.dtype}>" == kernel)
+    return sum(1 for l in wl.layers if layer_kernel_name(l.cin, l.cout, l.stride, wl.dtype) == kernel)
 
 
 def _csv_rows(path):
@@ -230,12 +241,44 @@ def digest_trace(path: str, steps: int, warmup: int, wl) -> str:
         n = launches_per_stride(k, wl)
         if n == 0:
             continue
-        first = 0 if k.endswith("vanished>") else 1   # no vanish pass on a full window
+        if wl.name in S.PFNS:
+            first = S.PFNS[wl.name].window             # batches of the first window
+        else:
+            first = 0 if k.endswith("vanished>") else 1   # no vanish pass on a full window
         span = (first + warmup + steps) * n            # launches of one pass
         a0, a1 = (first + warmup) * n, (first + warmup + steps) * n
         b0, b1 = 2 * span + a0, 2 * span + a1          # third pass: events stamped by every launch
         if len(v) >= b1:
             out.append(f"| {k} | {statistics.fmean(v[a0:a1]):.2f} | {statistics.fmean(v[b0:b1]):.2f} |")
+    return "\n".join(out)
+
+
+def digest_sweep_trace(path: str, steps: int, warmup: int) -> str:
+    """Per sweep shape, the layer kernel's rocprofv3 duration over the timed
+    strides and over the event-timed pass of a --kernel-trace csv of
+    `bench.py --sweep` (per shape: the timed pass, the event-timed pass, then
+    10 full recomputes)."""
+    rows = sorted(_csv_rows(path), key=lambda r: int(r["Start_Timestamp"]))
+    by = {}
+    for r in rows:
+        by.setdefault(short_kernel(r["Kernel_Name"]), []).append(
+            (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    span = 1 + warmup + steps
+    out = ["| Cin | Cout | layer kernel | timed strides: avg (us) | event-timed pass: avg (us) | full recompute: avg (us) |",
+           "|---|---|---|---|---|---|"]
+    for ci in S.SWEEP_CIN:
+        for co in S.SWEEP_COUT:
+            k = layer_kernel_name(ci, co, 1, "f32")
+            v = by.get(k, [])
+            if len(v) < 2 * span:
+                continue
+            out.append(f"| {ci} | {co} | {k} | {statistics.fmean(v[1 + warmup:span]):.2f} | "
+                       f"{statistics.fmean(v[span + 1 + warmup:2 * span]):.2f} | "
+                       f"{statistics.fmean(v[2 * span:]):.2f} |")
+    for k in sorted(by):
+        if k.startswith("detect_kernel"):
+            v = by[k]
+            out.append(f"| all | all | {k} | {statistics.fmean(v):.2f} (every launch) | | |")
     return "\n".join(out)
 
 
@@ -386,7 +429,10 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.digest_trace:
-        print(digest_trace(args.digest_trace, args.steps, args.warmup, S.workload(args.workload)))
+        if args.sweep:
+            print(digest_sweep_trace(args.digest_trace, args.steps, args.warmup))
+        else:
+            print(digest_trace(args.digest_trace, args.steps, args.warmup, S.workload(args.workload)))
         return 0
     if args.digest_pmc:
         per = launches_per_stride(args.kernel, S.workload(args.workload))
