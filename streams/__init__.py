@@ -53,6 +53,7 @@ class LayerSpec:
     cout: int
     stride: int
     relu: bool
+    sub: bool = False       # submanifold convolution (sparse workloads)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -76,6 +77,15 @@ def _block(cin: int, f: int, n: int) -> List[LayerSpec]:
 
 
 _BACKBONE = tuple(_block(64, 64, 4) + _block(64, 128, 6) + _block(128, 256, 6))
+
+
+def _sparse_block(cin: int, f: int, n: int) -> List[LayerSpec]:
+    """Sparse PointPillars block: a regular sparse stride-2 conv, then n-1
+    submanifold convs (Sec. III-E)."""
+    return [LayerSpec(cin, f, 2, True)] + [LayerSpec(f, f, 1, True, True) for _ in range(n - 1)]
+
+
+_SPARSE_BACKBONE = tuple(_sparse_block(64, 64, 4) + _sparse_block(64, 128, 6) + _sparse_block(128, 256, 6))
 
 # Single-layer channel sweep at the paper's drone-LiDAR sparsity: one 3x3
 # stride-1 conv, Cin in {16, 32, 64, 128} x Cout in {8, 16, 32, 64, 128}, on a
@@ -107,6 +117,14 @@ WORKLOADS = {
     "c5": Workload("c5", 1024, 1024, 64, "f32", tuple(_block(64, 64, 4)), 100, 48000,
                    "1024x1024 drone grid, block 1, 4 concurrent streams"),
     **_sweep_workloads(),
+    # sparse backbones on the toggling 432x496 stream (18 degree sectors, 60
+    # pillars appear and 60 vanish per stride): the active sets move
+    "s2": Workload("s2", 496, 432, 64, "f32", tuple(_sparse_block(64, 64, 4)), 100, 16000,
+                   "sparse block 1 (regular s2 + 3 submanifold, 64 ch) on 432x496 with toggles"),
+    "s3": Workload("s3", 496, 432, 64, "f32", _SPARSE_BACKBONE, 100, 16000,
+                   "sparse 3-block backbone (regular + submanifold), fp32, 432x496 with toggles"),
+    "s4": Workload("s4", 496, 432, 64, "bf16", _SPARSE_BACKBONE, 200, 16000,
+                   "sparse 3-block backbone in bf16, 18 deg strides + 1% toggles"),
     "p2": Workload("p2", 504, 504, 64, "f32", tuple(_block(64, 64, 4)), 100, 254016,
                    "points of the 504x504 drone scan -> incremental pillar feature net (9 -> 64) -> "
                    "PointPillars block 1"),
@@ -150,6 +168,8 @@ def _family(name: str) -> int:
         return 6
     if name.startswith("p"):
         return 7
+    if name.startswith("s"):
+        return 4            # the toggling stream of c4
     return int(name[1])
 
 
@@ -224,7 +244,7 @@ def weights(name: str) -> List[np.ndarray]:
     representable in bfloat16).
     """
     wl = workload(name)
-    family = {"c1": 1, "c2": 2, "c3": 2, "c4": 2, "c5": 5}.get(name, 6)
+    family = {"c1": 1, "c2": 2, "c3": 2, "c4": 2, "c5": 5, "s2": 2, "s3": 2, "s4": 2}.get(name, 6)
     out = []
     for li, ls in enumerate(wl.layers):
         key = (WEIGHT_SEED, family, li) if family != 6 else (WEIGHT_SEED, family, ls.cin, ls.cout)
@@ -378,9 +398,9 @@ class Stream:
         if name == "c1":
             occ = np.sort(scene_rng.choice(self.HW, size=400, replace=False))
             self.n_sectors = 10
-        elif name in ("c2", "c3", "c4"):
+        elif name in ("c2", "c3", "c4", "s2", "s3", "s4"):
             occ = self._scene_432x496(scene_rng)
-            self.n_sectors = 20 if name == "c4" else 10
+            self.n_sectors = 10 if name in ("c2", "c3") else 20
         elif name == "c5":
             occ = self._scene_1024(scene_rng)
             self.n_sectors = 20
@@ -498,7 +518,7 @@ class Stream:
             self.feat[off] = 0.0
             self.occ[on] = True
             self._fill(on, rng)
-        elif self.name == "c4":
+        elif self.name in ("c4", "s2", "s3", "s4"):
             self._fill(np.flatnonzero(self.occ & in_sec), rng)
             occ_sec = np.flatnonzero(self.occ & in_sec)
             emp_sec = np.flatnonzero(~self.occ & in_sec)
