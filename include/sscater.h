@@ -203,6 +203,26 @@ int sscater_create_pfn(const sscater_grid* grid, const sscater_layer* layers, in
  * SSCATER_E_OVERFLOW when n_points > max_new_points.  Asynchronous. */
 int sscater_step_points(sscater_t h, const float* points, int32_t n_points, void* stream);
 
+/* A sparse backbone (Sec. III-E; the submanifold operator of Sec. II-B):
+ * layers and weights as for sscater_create, plus submanifold[n_layers] (host,
+ * 0 or 1 per layer).  The input is a sparse tensor whose active sites are the
+ * stride's pillars (whatever their values); a regular layer
+ * (submanifold[l] = 0) is a sparse convolution whose active output sites are
+ * those with an active input site in their receptive field, a submanifold
+ * layer (submanifold[l] = 1, stride 1) keeps its input's active sites; every
+ * output is phi(conv) at its active sites and zero elsewhere.  Layer 1 must
+ * be regular.  A changed set: A_0 gains the pillars that appeared or
+ * vanished; A_l holds the sites of the receptive-field rule over A_{l-1} that
+ * are active now or were in the previous stride (sscater_changed), while
+ * sscater_stats counts each layer's work list (all sites of the rule, whose
+ * maps are kept current so that a site joining the active set holds its
+ * value).  Dense-mode steps are refused.  The stride counter behind the
+ * active sets is 31 bits wide.  Errors as sscater_create, plus
+ * SSCATER_E_INVALID_ARG for a null submanifold array, a submanifold first
+ * layer or a submanifold layer with stride 2. */
+int sscater_create_sparse(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
+                          const void* const* weights, const int32_t* submanifold, sscater_t* out);
+
 /* Advance by one stride (Alg. 1): detect the changed input cells, then for
  * each layer scatter the deltas into the persistent maps (Eq. 2) and build the
  * next layer's change list.  The first step after create/reset is the full

@@ -42,6 +42,10 @@ struct LayerState {
     uint32_t* stamp = nullptr;
     int32_t* list = nullptr; // NSHARD segments of Hout*Wout cells
     void* delta = nullptr;   // deltas of this layer's output, dense by cell (nullptr for the last layer)
+    // sparse backbones: the output active-set words (owned by a regular
+    // layer, shared with the submanifold layers of its block)
+    uint64_t* memb = nullptr;
+    bool sub = false;
 };
 
 // One upsampler of the neck.
@@ -91,6 +95,7 @@ struct sscater {
     long long* cum = nullptr;      // running totals, same layout as one set
     int32_t* err_host = nullptr;   // host-visible sticky error word
     int32_t* err_dev = nullptr;
+    bool sparse = false;           // regular sparse + submanifold layers
     // points mode: the incremental pillar feature net in front of the layers
     bool pfn = false;
     sscater_pfn pfn_spec{};
@@ -234,13 +239,23 @@ int run_layers(sscater* h, int set, uint32_t epoch, hipStream_t s) {
         a.epoch = epoch;
         a.has_next = l < h->L;
         if (a.has_next) a.next = prop_target(h, l + 1, set);
+        if (h->sparse) {
+            a.memb = ls.memb;
+            if (!ls.sub)      // a regular layer passes its membership changes to the next regular layer
+                for (int k = l + 1; k <= h->L; ++k)
+                    if (!h->layers[k - 1].sub) {
+                        const LayerState& nx = h->layers[k - 1];
+                        a.mnext = MembTarget{nx.memb, nx.spec.stride, nx.Hout, nx.Wout};
+                        break;
+                    }
+        }
         if (l == h->L) {
             a.cum_src = cnt;
             a.cum_dst = h->cum;
             a.n_cum = h->ncnt();
         }
         e = timed_launch(h, 1 + l, s, [&](const LaunchCtx& c) {
-            return launch_layer(a, ls.spec.cin, ls.spec.cout, ls.spec.stride, h->bf16, h->layer_grid, c);
+            return launch_layer(a, ls.spec.cin, ls.spec.cout, ls.spec.stride, h->bf16, h->sparse, h->layer_grid, c);
         });
         if (e != hipSuccess) return hip_fail(e);
     }
@@ -448,6 +463,7 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
     const long long cells = (long long)h->grid.H * h->grid.W;
     // NULL idx with count == H*W is dense mode; NULL idx with count 0 is an empty stride
     const bool dense = pl->idx == nullptr && pl->count != 0;
+    if (dense && h->sparse) return SSCATER_E_INVALID_ARG;   // the pillar set is part of a sparse input
     if (dense) {
         if (pl->count != cells || !pl->feats) return SSCATER_E_INVALID_ARG;
     } else {
@@ -481,6 +497,10 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
     d.epoch = epoch;
     d.err = h->err_dev;
     d.next = prop_target(h, 1, set);
+    if (h->sparse) {
+        const LayerState& l1 = h->layers[0];
+        d.memb = MembTarget{l1.memb, l1.spec.stride, l1.Hout, l1.Wout};
+    }
     hipError_t e = timed_launch(h, 0, s, [&](const LaunchCtx& c) { return launch_detect_present(d, h->row_bytes, h->bf16, c); });
     if (e != hipSuccess) return hip_fail(e);
 
@@ -647,6 +667,38 @@ int sscater_step_points(sscater_t h, const float* points, int32_t n_points, void
     return SSCATER_OK;
 }
 
+int sscater_create_sparse(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
+                          const void* const* weights, const int32_t* submanifold, sscater_t* out) {
+    if (!grid || !layers || !submanifold || !out || n_layers < 1 || n_layers > SSCATER_MAX_LAYERS)
+        return SSCATER_E_INVALID_ARG;
+    *out = nullptr;
+    if (submanifold[0] != 0) return SSCATER_E_INVALID_ARG;   // a sparse stack starts with a regular layer
+    for (int l = 0; l < n_layers; ++l)
+        if ((submanifold[l] != 0 && submanifold[l] != 1) || (submanifold[l] == 1 && layers[l].stride != 1))
+            return SSCATER_E_INVALID_ARG;
+    sscater_t h = nullptr;
+    int rc = sscater_create_neck(grid, layers, n_layers, weights, nullptr, 0, nullptr, &h);
+    if (rc != SSCATER_OK) return rc;
+    DeviceGuard dg(h->device);
+    if (!dg.ok) {
+        sscater_destroy(h);
+        return hip_fail(hipGetLastError());
+    }
+    for (int l = 0; l < n_layers; ++l) {
+        LayerState& ls = h->layers[l];
+        ls.sub = submanifold[l] == 1;
+        if (ls.sub) {
+            ls.memb = h->layers[l - 1].memb;
+        } else if ((rc = dev_alloc(h, (void**)&ls.memb, (size_t)ls.Hout * ls.Wout * 8)) != SSCATER_OK) {
+            sscater_destroy(h);
+            return rc;
+        }
+    }
+    h->sparse = true;
+    *out = h;
+    return SSCATER_OK;
+}
+
 int sscater_read(sscater_t h, int32_t layer, void* dst, size_t dst_bytes, void* stream) {
     if (!h || !dst || layer < 0 || layer > h->L + (h->n_ups > 0 ? 1 : 0)) return SSCATER_E_INVALID_ARG;
     if (int rc = check_sticky(h)) return rc;
@@ -673,7 +725,9 @@ int sscater_read(sscater_t h, int32_t layer, void* dst, size_t dst_bytes, void* 
     const LayerState& ls = h->layers[layer - 1];
     const long long n = (long long)ls.Hout * ls.Wout * ls.spec.cout;
     if (dst_bytes < (size_t)n * esz) return SSCATER_E_INVALID_ARG;
-    hipError_t e = launch_read(ls.Z, dst, n, ls.spec.relu, h->bf16, s);
+    hipError_t e = h->sparse ? launch_read_masked(ls.Z, dst, (long long)ls.Hout * ls.Wout, ls.spec.cout, ls.memb,
+                                                  ls.spec.relu, h->bf16, s)
+                             : launch_read(ls.Z, dst, n, ls.spec.relu, h->bf16, s);
     return e == hipSuccess ? SSCATER_OK : hip_fail(e);
 }
 
@@ -695,6 +749,10 @@ int sscater_reset(sscater_t h, void* stream) {
     if (e == hipSuccess && h->Zn) e = launch_fill_zero(h->Zn, round_up((size_t)h->Hn * h->Wn * h->Cn * 4, 256), s);
     if (e == hipSuccess) e = launch_fill_zero(h->counters, round_up((size_t)2 * h->ncnt() * 4, 256), s);
     if (e == hipSuccess) e = launch_fill_zero(h->cum, round_up((size_t)h->ncnt() * 8, 256), s);
+    for (int l = 0; l < h->L && e == hipSuccess && h->sparse; ++l) {
+        const LayerState& ls = h->layers[l];
+        if (!ls.sub) e = launch_fill_zero(ls.memb, round_up((size_t)ls.Hout * ls.Wout * 8, 256), s);
+    }
     if (e == hipSuccess && h->pfn) {
         const size_t slots = (size_t)h->pfn_spec.window + 1;
         e = launch_fill_zero(h->head, round_up(cells * 4, 256), s);
@@ -760,6 +818,23 @@ int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32
             e = hipMemcpy(buf.data() + at, ls.list + (size_t)k * cap_cells, (size_t)m * 4, hipMemcpyDeviceToHost);
             if (e != hipSuccess) return hip_fail(e);
         }
+    }
+    if (h->sparse && layer >= 1 && layer <= h->L && !buf.empty()) {
+        // a sparse layer's changed sites: its work list minus the sites that
+        // are active neither now nor in the previous stride
+        const LayerState& ls = h->layers[layer - 1];
+        std::vector<uint64_t> mw((size_t)ls.Hout * ls.Wout);
+        e = hipMemcpy(mw.data(), ls.memb, mw.size() * 8, hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(e);
+        const uint64_t ep = h->last_epoch & 0x7FFFFFFFu;
+        size_t k = 0;
+        for (int32_t q : buf) {
+            const uint64_t w = mw[(size_t)q];
+            const bool now = (uint32_t)w != 0u;
+            const bool prev = (w >> 33) == ep ? ((w >> 32) & 1ull) != 0ull : now;
+            if (now || prev) buf[k++] = q;
+        }
+        buf.resize(k);
     }
     const int32_t n = (int32_t)buf.size();
     *count_host = n;

@@ -25,7 +25,7 @@
 
 namespace ssc {
 
-template <int ROWB, bool BF16, bool VANISH>
+template <int ROWB, bool BF16, bool VANISH, bool SPARSE>
 __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
     constexpr int G = ROWB / 16;   // lanes per feature row
     constexpr int PPW = 64 / G;    // rows per wavefront pass
@@ -61,6 +61,11 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
         // outstanding loads where the branch ends.
         const int pc = act ? p : 0;
         const uint64_t mine = ((uint64_t)a.epoch << 32) | (uint32_t)i;
+        // sparse backbones: the pillar set itself is an input; a pillar whose
+        // cell had none in the previous stride appeared (the word was
+        // written by an earlier stride, or never)
+        uint64_t op = 0ull;
+        if (SPARSE && !VANISH) op = a.pres[pc];
         uint32_t st = 0u;
         int c = 0;              // vanish mode: cell of row i of the new list
         uint64_t cw = 0ull;     // and its presence word
@@ -84,7 +89,9 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
             if (a.chk_idx && sub == 0 && i < a.chk_count && c >= 0 && c < a.HW && cw != mine)
                 flag_error(a.err, ERR_DUPLICATE);
         }
-        const bool d = act && (nv.x != ov.x || nv.y != ov.y || nv.z != ov.z || nv.w != ov.w);
+        bool tog = false;       // sparse backbones: the pillar appeared or vanished
+        if (SPARSE) tog = VANISH ? act : (act && (op == 0ull || (uint32_t)(op >> 32) != a.epoch - 1u));
+        const bool d = act && (tog || nv.x != ov.x || nv.y != ov.y || nv.z != ov.z || nv.w != ov.w);
         const unsigned long long bal = __ballot(d);
         const unsigned long long gm = (G == 64 ? ~0ull : ((1ull << G) - 1ull)) << gbase;
         const bool gd = (bal & gm) != 0ull;
@@ -107,6 +114,7 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
             *reinterpret_cast<uint4*>(xrow) = nv;
             if (sub == 0) a.stamp0[p] = a.epoch;
         }
+        if (SPARSE && tog && sub == 0) memb_spread(a.memb, p, a.next.Win, VANISH ? -1 : 1, a.epoch);
         // |A_0|: one counter per shard, no returned value to wait for
         const int changed = (int)__popcll(__ballot(gd && sub == 0));
         if (lane == 0 && changed) atomicAdd(a.count0 + shard * CSTRIDE, changed);
@@ -125,10 +133,14 @@ static hipError_t launch_detect(const DetectArgs& a, int row_bytes, bool bf16, c
     if (blocks < 1) blocks = 1;
     if (blocks > 4096) blocks = 4096;
     dim3 grid((unsigned)blocks), block(256);
-#define SSC_DETECT_CASE(RB)                                                                      \
-    case RB:                                                                                     \
-        return bf16 ? launch_kernel(c, detect_kernel<RB, true, VANISH>, grid, block, a)          \
-                    : launch_kernel(c, detect_kernel<RB, false, VANISH>, grid, block, a);
+    const bool sp = a.memb.memb != nullptr;
+#define SSC_DETECT_CASE(RB)                                                                             \
+    case RB:                                                                                            \
+        if (sp)                                                                                         \
+            return bf16 ? launch_kernel(c, detect_kernel<RB, true, VANISH, true>, grid, block, a)       \
+                        : launch_kernel(c, detect_kernel<RB, false, VANISH, true>, grid, block, a);     \
+        return bf16 ? launch_kernel(c, detect_kernel<RB, true, VANISH, false>, grid, block, a)          \
+                    : launch_kernel(c, detect_kernel<RB, false, VANISH, false>, grid, block, a);
     switch (row_bytes) {
         SSC_DETECT_CASE(16)
         SSC_DETECT_CASE(32)

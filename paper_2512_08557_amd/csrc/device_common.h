@@ -95,6 +95,46 @@ __device__ __forceinline__ void prop_finish(const PropTarget& t, uint32_t epoch,
     }
 }
 
+// Active-set words (sparse backbones): see MembTarget.
+__device__ __forceinline__ bool memb_now(uint64_t w) { return (uint32_t)w != 0u; }
+
+__device__ __forceinline__ bool memb_prev(uint64_t w, uint32_t epoch) {
+    return (uint32_t)(w >> 33) == (epoch & 0x7FFFFFFFu) ? ((w >> 32) & 1ull) != 0ull : memb_now(w);
+}
+
+// Adds delta to the site's count; the first change of a stride records the
+// membership the site had before it.  Lock-free: a failed compare-and-swap
+// means another lane changed the word, and the loop retries on its value.
+__device__ __forceinline__ void memb_add(uint64_t* p, int delta, uint32_t epoch) {
+    const unsigned long long ep = epoch & 0x7FFFFFFFu;
+    unsigned long long old = __hip_atomic_load(reinterpret_cast<unsigned long long*>(p), __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+    for (;;) {
+        const uint32_t cnt = (uint32_t)old;
+        const unsigned long long was = ((old >> 33) == ep) ? ((old >> 32) & 1ull) : (cnt != 0u ? 1ull : 0ull);
+        const unsigned long long nw = (ep << 33) | (was << 32) | (unsigned long long)(uint32_t)(cnt + (uint32_t)delta);
+        const unsigned long long got = atomicCAS(reinterpret_cast<unsigned long long*>(p), old, nw);
+        if (got == old) return;
+        old = got;
+    }
+}
+
+// Counts of the next regular layer: +-1 at every output site whose receptive
+// field holds `cell` (the same stride rule as the change lists).
+__device__ __forceinline__ void memb_spread(const MembTarget& t, int cell, int win, int delta, uint32_t epoch) {
+    const int i = cell / win, j = cell - (cell / win) * win;
+    for (int k = 0; k < 9; ++k) {
+        int rn = i - k / 3 + 1, cn = j - k % 3 + 1;
+        if (t.stride == 2) {
+            if ((rn | cn) & 1) continue;
+            rn >>= 1;
+            cn >>= 1;
+        }
+        if (rn < 0 || rn >= t.Hout || cn < 0 || cn >= t.Wout) continue;
+        memb_add(t.memb + (size_t)rn * t.Wout + cn, delta, epoch);
+    }
+}
+
 // fp32 -> bf16 bits, round to nearest even (finite values).
 __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
     uint32_t u = __float_as_uint(f);

@@ -84,8 +84,11 @@ __device__ __forceinline__ void mfma_chunk(f4v (&acc)[NCB], const uint4 av, cons
 // Z update and next-layer delta row of one lane: output cell q, output
 // channels co0 .. co0+3 (fp32 Z_new = Z_old + D; delta phi(Z_new) -
 // phi(Z_old), or the bf16 pair [bf16(phi(Z_new)) | bf16(phi(Z_old))]).
+// Sparse backbones: now / prev say whether the site is active in this and
+// in the previous stride; an inactive site's output is zero.
 template <int COUT, bool BF16>
-__device__ __forceinline__ void epilogue4(const LayerArgs& a, int q, int co0, const f4v o, const f4v d) {
+__device__ __forceinline__ void epilogue4(const LayerArgs& a, int q, int co0, const f4v o, const f4v d,
+                                          bool now = true, bool prev = true) {
     f4v zn;
     zn.x = o.x + d.x;
     zn.y = o.y + d.y;
@@ -98,6 +101,8 @@ __device__ __forceinline__ void epilogue4(const LayerArgs& a, int q, int co0, co
         yo.x = fmaxf(yo.x, 0.f); yo.y = fmaxf(yo.y, 0.f); yo.z = fmaxf(yo.z, 0.f); yo.w = fmaxf(yo.w, 0.f);
         yn.x = fmaxf(yn.x, 0.f); yn.y = fmaxf(yn.y, 0.f); yn.z = fmaxf(yn.z, 0.f); yn.w = fmaxf(yn.w, 0.f);
     }
+    if (!prev) yo = f4v{0.f, 0.f, 0.f, 0.f};
+    if (!now) yn = f4v{0.f, 0.f, 0.f, 0.f};
     char* drow = static_cast<char*>(a.delta_out) + (size_t)q * (4 * COUT);
     if constexpr (BF16) {
         uint2 pn, po;
@@ -117,7 +122,7 @@ __device__ __forceinline__ void epilogue4(const LayerArgs& a, int q, int co0, co
     }
 }
 
-template <int CIN, int COUT, int S, bool BF16>
+template <int CIN, int COUT, int S, bool BF16, bool SPARSE>
 __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerArgs a) {
     constexpr int NCBT = LayerShape<COUT>::NCBT;
     constexpr int NCB = LayerShape<COUT>::NCB;
@@ -178,10 +183,18 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb)
             zo[cb] = *reinterpret_cast<const f4v*>(zrow + min((cw * NCB + cb) * 16 + 4 * g, COUT - 4));
+        // sparse backbones: only a site active now or before can change, and
+        // only such sites go to the next layer's list
+        bool now = true, prev = true;
+        if constexpr (SPARSE) {
+            const uint64_t mw = a.memb[q];
+            now = memb_now(mw);
+            prev = memb_prev(mw, a.epoch);
+        }
         // next layer's change list: stamp the footprint in the same round trip
         // as the stamp and map loads, append the new cells at the end
         PropBatch<4> pb;
-        if (do_prop) prop_issue<4, false>(a.next, q, vrow, g, a.epoch, pb);
+        if (do_prop) prop_issue<4, false>(a.next, q, vrow && (now || prev), g, a.epoch, pb);
         int rows[9];
         bool any[9];
 #pragma unroll
@@ -294,8 +307,12 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
                 const int co0 = (cw * NCB + cb) * 16 + 4 * g;
-                if (COUT % 16 == 0 || co0 < COUT) epilogue4<COUT, BF16>(a, q, co0, zo[cb], acc[cb]);
+                if (COUT % 16 == 0 || co0 < COUT) epilogue4<COUT, BF16>(a, q, co0, zo[cb], acc[cb], now, prev);
             }
+        }
+        if constexpr (SPARSE) {
+            if (a.mnext.memb && wave == 0 && g == 0 && vrow && now != prev)
+                memb_spread(a.mnext, q, a.Wout, now ? 1 : -1, a.epoch);
         }
         if (do_prop) prop_finish<4>(a.next, a.epoch, shard, pb);
 
@@ -330,7 +347,7 @@ struct WideShape {
     static constexpr int NH = NCBT / 2;                     // workgroups per tile pair
 };
 
-template <int CIN, int COUT, int S, bool BF16>
+template <int CIN, int COUT, int S, bool BF16, bool SPARSE>
 __global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
     using W = WideShape<CIN, COUT, BF16>;
     constexpr int NCH = W::NCH, NCBT = W::NCBT, NH = W::NH;
@@ -369,8 +386,14 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
             if (__ballot(rows[t] >= 0) != 0ull) mask |= 1u << t;
         }
         const f4v zo = *reinterpret_cast<const f4v*>(a.Z + (size_t)q * COUT + cbg * 16 + 4 * g);
+        bool now = true, prev = true;           // sparse backbones, as in the narrow kernel
+        if constexpr (SPARSE) {
+            const uint64_t mw = a.memb[q];
+            now = memb_now(mw);
+            prev = memb_prev(mw, a.epoch);
+        }
         PropBatch<4> pb;
-        if (do_prop) prop_issue<4, false>(a.next, q, vrow, g, a.epoch, pb);
+        if (do_prop) prop_issue<4, false>(a.next, q, vrow && (now || prev), g, a.epoch, pb);
         if (threadIdx.x == 0) tapmask = 0;
         __syncthreads();
         if (lane == 0 && mask) atomicOr(&tapmask, (int)mask);
@@ -423,7 +446,11 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
                 mfma_chunk<BF16, 1>(acc, av[c], bb);
             }
         }
-        if (vrow) epilogue4<COUT, BF16>(a, q, cbg * 16 + 4 * g, zo, acc[0]);
+        if (vrow) epilogue4<COUT, BF16>(a, q, cbg * 16 + 4 * g, zo, acc[0], now, prev);
+        if constexpr (SPARSE) {
+            if (a.mnext.memb && h == 0 && cbl == 0 && g == 0 && vrow && now != prev)
+                memb_spread(a.mnext, q, a.Wout, now ? 1 : -1, a.epoch);
+        }
         if (do_prop) prop_finish<4>(a.next, a.epoch, shard, pb);
         __syncthreads();                               // the stage buffers are free again
     }
@@ -447,7 +474,7 @@ bool layer_supported(int cin, int cout, int stride, bool /*bf16*/) {
     return false;
 }
 
-template <int CI, int CO, int S, bool BF16>
+template <int CI, int CO, int S, bool BF16, bool SPARSE>
 static hipError_t launch_shape(const LayerArgs& a, int grid, const LaunchCtx& c) {
     // wide layers: more than 8 input chunks, or more than 4 with at least 8
     // output blocks (a narrow workgroup would then run 2+ blocks x 72 steps
@@ -458,19 +485,24 @@ static hipError_t launch_shape(const LayerArgs& a, int grid, const LaunchCtx& c)
         constexpr int NH = WideShape<CI, CO, BF16>::NH;
         int gl = std::max(1, grid / (2 * NH * NSHARD));
         gl = std::min(gl, std::max(1, (a.cap + 31) / 32));
-        return launch_kernel(c, layer_kernel_wide<CI, CO, S, BF16>, dim3(gl * NH * NSHARD), dim3(256), a);
+        return launch_kernel(c, layer_kernel_wide<CI, CO, S, BF16, SPARSE>, dim3(gl * NH * NSHARD), dim3(256), a);
     } else {
         // whole runs of 4 tiles on every XCD for every segment
         grid = std::max(32 * NSHARD, grid / (32 * NSHARD) * (32 * NSHARD));
-        return launch_kernel(c, layer_kernel<CI, CO, S, BF16>, dim3(grid), dim3(64 * LayerShape<CO>::NW), a);
+        return launch_kernel(c, layer_kernel<CI, CO, S, BF16, SPARSE>, dim3(grid), dim3(64 * LayerShape<CO>::NW), a);
     }
 }
 
-hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, int grid,
+hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, bool sparse, int grid,
                         const LaunchCtx& c) {
 #define SSC_LAUNCH(CI, CO, S)                                                                               \
-    if (cin == CI && cout == CO && stride == S)                                                             \
-        return bf16 ? launch_shape<CI, CO, S, true>(a, grid, c) : launch_shape<CI, CO, S, false>(a, grid, c);
+    if (cin == CI && cout == CO && stride == S) {                                                           \
+        if (sparse)                                                                                         \
+            return bf16 ? launch_shape<CI, CO, S, true, true>(a, grid, c)                                   \
+                        : launch_shape<CI, CO, S, false, true>(a, grid, c);                                 \
+        return bf16 ? launch_shape<CI, CO, S, true, false>(a, grid, c)                                      \
+                    : launch_shape<CI, CO, S, false, false>(a, grid, c);                                    \
+    }
     SSC_ALL_SHAPES(SSC_LAUNCH)
 #undef SSC_LAUNCH
     return hipErrorInvalidValue;

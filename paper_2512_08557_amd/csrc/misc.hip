@@ -46,6 +46,30 @@ __global__ __launch_bounds__(256) void read_slice_kernel(const float* __restrict
     }
 }
 
+// phi(Z) at the active sites of a sparse layer, zero elsewhere.
+template <bool BF16>
+__global__ __launch_bounds__(256) void read_masked_kernel(const float* __restrict__ Z, void* __restrict__ dst,
+                                                          long long cells, int cout4, const uint64_t* __restrict__ memb,
+                                                          int relu) {
+    const long long n4 = cells * cout4;
+    for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n4;
+         i += (long long)gridDim.x * blockDim.x) {
+        f4v z = reinterpret_cast<const f4v*>(Z)[i];
+        if (relu) {
+            z.x = fmaxf(z.x, 0.f); z.y = fmaxf(z.y, 0.f); z.z = fmaxf(z.z, 0.f); z.w = fmaxf(z.w, 0.f);
+        }
+        if (!memb_now(memb[i / cout4])) z = f4v{0.f, 0.f, 0.f, 0.f};
+        if constexpr (BF16) {
+            uint2 p;
+            p.x = f32_to_bf16_bits(z.x) | (f32_to_bf16_bits(z.y) << 16);
+            p.y = f32_to_bf16_bits(z.z) | (f32_to_bf16_bits(z.w) << 16);
+            reinterpret_cast<uint2*>(dst)[i] = p;
+        } else {
+            reinterpret_cast<f4v*>(dst)[i] = z;
+        }
+    }
+}
+
 __global__ __launch_bounds__(256) void fill_zero_kernel(uint4* __restrict__ p, long long n16) {
     for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n16;
          i += (long long)gridDim.x * blockDim.x)
@@ -64,6 +88,18 @@ hipError_t launch_read(const float* Z, void* dst, long long n, int relu, bool bf
     const long long n4 = n / 4;
     if (bf16) hipLaunchKernelGGL(read_kernel<true>, dim3(grid_for(n4)), dim3(256), 0, s, Z, dst, n4, relu);
     else hipLaunchKernelGGL(read_kernel<false>, dim3(grid_for(n4)), dim3(256), 0, s, Z, dst, n4, relu);
+    return hipGetLastError();
+}
+
+hipError_t launch_read_masked(const float* Z, void* dst, long long cells, int cout, const uint64_t* memb, int relu,
+                              bool bf16, hipStream_t s) {
+    const long long n4 = cells * (cout / 4);
+    if (bf16)
+        hipLaunchKernelGGL(read_masked_kernel<true>, dim3(grid_for(n4)), dim3(256), 0, s, Z, dst, cells, cout / 4, memb,
+                           relu);
+    else
+        hipLaunchKernelGGL(read_masked_kernel<false>, dim3(grid_for(n4)), dim3(256), 0, s, Z, dst, cells, cout / 4,
+                           memb, relu);
     return hipGetLastError();
 }
 

@@ -33,6 +33,23 @@ struct PropTarget {
     int32_t* pairs;       // (input, output) pairs of the consuming layer, same layout
 };
 
+// Sparse backbones (regular sparse and submanifold convolutions): every
+// layer's output sites carry an active-set word,
+//   bits 0..31  number of active input sites in the site's receptive field
+//               (the site is active while it is not zero),
+//   bit 32      whether the site was active at the end of the previous stride,
+//   bits 33..63 the epoch (mod 2^31) of the word's last change,
+// so both the current and the previous active set are read from one word.
+// A submanifold layer shares the word array of the regular layer that starts
+// its block (it keeps the active set).  Membership changes go one level down:
+// pillar toggles update the first regular layer's words, a regular layer's
+// kernel updates the next regular layer's words for its sites that changed.
+struct MembTarget {
+    uint64_t* memb;       // words of the next regular layer's output grid (nullptr: none)
+    int stride;           // that layer's stride
+    int Hout, Wout;       // its output grid (its input grid is the source grid)
+};
+
 // Changed-cell detection on the input canvas.
 struct DetectArgs {
     const int32_t* idx;   // pillar cell indices (nullptr: dense mode, cell = i)
@@ -53,6 +70,7 @@ struct DetectArgs {
     uint32_t epoch;
     int32_t* err;         // sticky error flags (host-visible memory)
     PropTarget next;
+    MembTarget memb;      // sparse backbones: the first layer's active-set words
 };
 
 // One convolution layer: contraction of the input deltas with the weights,
@@ -72,6 +90,10 @@ struct LayerArgs {
     uint32_t epoch;
     int has_next;
     PropTarget next;
+    // sparse backbones: this layer's output active-set words, and where a
+    // regular layer sends its sites' membership changes
+    const uint64_t* memb;
+    MembTarget mnext;
     // running totals, folded in by the last layer of a stride
     const int32_t* cum_src;     // this stride's counters [n_cum]
     long long* cum_dst;         // totals [n_cum]
@@ -166,9 +188,12 @@ inline hipError_t launch_kernel(const LaunchCtx& c, K kernel, dim3 grid, dim3 bl
 hipError_t launch_detect_present(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c);
 hipError_t launch_detect_vanished(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c);
 bool layer_supported(int cin, int cout, int stride, bool bf16);
-hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, int grid,
+hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, bool sparse, int grid,
                         const LaunchCtx& c);
 hipError_t launch_read(const float* Z, void* dst, long long n, int relu, bool bf16, hipStream_t s);
+// phi(Z) with the sites outside the active set (sparse backbones) zeroed.
+hipError_t launch_read_masked(const float* Z, void* dst, long long cells, int cout, const uint64_t* memb, int relu,
+                              bool bf16, hipStream_t s);
 // phi of channels [coff, coff + cout) of a [cells][ctot] map into the same
 // channels of a [cells][ctot] destination.
 hipError_t launch_read_slice(const float* Z, void* dst, long long cells, int ctot, int coff, int cout, int relu,

@@ -23,7 +23,8 @@ OK, E_INVALID_ARG, E_OUT_OF_MEMORY, E_HIP, E_OVERFLOW, E_DEVICE = 0, -1, -2, -3,
 F32, BF16 = 0, 1
 
 # every function declared in include/sscater.h
-EXPORTS = ("sscater_create", "sscater_create_neck", "sscater_create_pfn", "sscater_step", "sscater_step_points",
+EXPORTS = ("sscater_create", "sscater_create_neck", "sscater_create_pfn", "sscater_create_sparse", "sscater_step",
+           "sscater_step_points",
            "sscater_read", "sscater_reset", "sscater_destroy", "sscater_changed", "sscater_stats", "sscater_profile",
            "sscater_profile_read", "sscater_strerror")
 
@@ -85,6 +86,8 @@ def lib() -> ctypes.CDLL:
         L.sscater_create_pfn.argtypes = [ctypes.POINTER(Grid), ctypes.POINTER(Layer), i32,
                                          ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(Pfn),
                                          ctypes.POINTER(ctypes.c_float), ctypes.POINTER(vp)]
+        L.sscater_create_sparse.argtypes = [ctypes.POINTER(Grid), ctypes.POINTER(Layer), i32,
+                                            ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(i32), ctypes.POINTER(vp)]
         L.sscater_step.argtypes = [vp, ctypes.POINTER(Pillars), vp]
         L.sscater_step_points.argtypes = [vp, vp, i32, vp]
         L.sscater_read.argtypes = [vp, i32, vp, ctypes.c_size_t, vp]
@@ -130,13 +133,14 @@ class Engine:
     def __init__(self, H: int, W: int, C0: int, layers: Sequence[Tuple[int, int, int, bool]],
                  weights: Sequence[np.ndarray], dtype: str = "f32", max_pillars: int = 16000,
                  ups: Sequence[Tuple[int, int, int, bool]] = (), up_weights: Sequence[np.ndarray] = (),
-                 pfn=None, pfn_weights: Optional[np.ndarray] = None):
+                 pfn=None, pfn_weights: Optional[np.ndarray] = None, submanifold: Optional[Sequence[bool]] = None):
         """layers: (cin, cout, stride, relu); weights: OIHW per layer.  ups:
         optional neck, (src_layer, cout, stride, relu) per upsampler with
         [cin, cout, s, s] weights; the neck map is layer len(layers) + 1.
         pfn: optional points mode, (x_min, y_min, res, max_points, window,
         max_new_points) with [C0, 9] float32 pfn_weights; strides are then
-        given to step_points."""
+        given to step_points.  submanifold: optional per-layer flags of a
+        sparse backbone (regular sparse layers where False)."""
         import torch  # device memory and streams only
         self._torch = torch
         self.H, self.W, self.C0 = H, W, C0
@@ -157,7 +161,16 @@ class Engine:
         handle = ctypes.c_void_p()
         self.ups = [tuple(u) for u in ups]
         self.pfn = tuple(pfn) if pfn is not None else None
-        if self.pfn is not None:
+        self.submanifold = [bool(x) for x in submanifold] if submanifold is not None else None
+        if self.submanifold is not None:
+            if self.ups or self.pfn is not None:
+                raise ValueError("a sparse backbone takes no neck and no points mode")
+            if len(self.submanifold) != n:
+                raise ValueError("one submanifold flag per layer")
+            flags = (ctypes.c_int32 * n)(*[int(x) for x in self.submanifold])
+            _check(lib().sscater_create_sparse(ctypes.byref(grid), larr, n, wptrs, flags, ctypes.byref(handle)),
+                   "sscater_create_sparse")
+        elif self.pfn is not None:
             if self.ups:
                 raise ValueError("points mode takes no neck")
             pw = np.ascontiguousarray(pfn_weights, dtype=np.float32)

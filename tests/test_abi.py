@@ -202,3 +202,30 @@ def test_create_pfn_rejects_invalid_arguments(case):
 
 def test_points_calls_reject_null_handle():
     assert ssc.lib().sscater_step_points(None, None, 0, None) == ssc.E_INVALID_ARG
+
+
+@pytest.mark.parametrize("case", ["null_flags", "first_sub", "sub_stride2", "flag2", "bad_layers"])
+def test_create_sparse_rejects_invalid_arguments(case):
+    """Every check runs on the host before any HIP call."""
+    lib = ssc.lib()
+    g = E.Grid(16, 16, 64, 100, E.F32)
+    L = [E.Layer(64, 64, 3, 2, 1, 1), E.Layer(64, 64, 3, 1, 1, 1), E.Layer(64, 64, 3, 1, 1, 1)]
+    flags = [0, 1, 1]
+    if case == "first_sub":
+        flags = [1, 1, 1]
+    elif case == "sub_stride2":
+        L[2].stride = 2
+    elif case == "flag2":
+        flags = [0, 2, 1]
+    elif case == "bad_layers":
+        L[1].cin = 32
+    n = len(L)
+    larr = (E.Layer * n)(*L)
+    bufs = [np.zeros((l.cout, l.cin, 3, 3), np.float32) for l in L]
+    wp = (ctypes.c_void_p * n)(*[b.ctypes.data for b in bufs])
+    fl = None if case == "null_flags" else (ctypes.c_int32 * n)(*flags)
+    h = ctypes.c_void_p()
+    rc = lib.sscater_create_sparse(ctypes.byref(g), larr, n, wp, fl, ctypes.byref(h))
+    if rc == ssc.OK:
+        lib.sscater_destroy(h)
+    assert rc == ssc.E_INVALID_ARG

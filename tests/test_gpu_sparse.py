@@ -1,0 +1,141 @@
+"""GPU parity of sparse backbones (a regular sparse convolution at each block
+input, then submanifold convolutions) against the CPU oracle, through the C
+ABI, on streams whose pillar sets change: every layer's change list bit for
+bit at every stride, the maps within 1e-4 * max|ref| (fp32) or 2e-2 (bf16)."""
+import numpy as np
+import pytest
+
+import oracle
+import streams as S
+from gpu_util import canvas_bits, check_lists, check_maps, note, read_map, to_device
+from oracle import sparse as SP
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+@pytest.fixture(autouse=True)
+def _announce(request):
+    note(f"[gpu-test] start {request.node.nodeid}")
+    yield
+    torch.cuda.synchronize()
+
+
+def _engine(H, W, C0, layers, ws, sub, dtype, max_pillars):
+    from paper_2512_08557_amd import Engine
+    return Engine(H, W, C0, layers, ws, dtype=dtype, max_pillars=max_pillars, submanifold=sub)
+
+
+def _run(name, n_strides, map_every):
+    wl = S.workload(name)
+    ws = S.weights(name)
+    layers = [(l.cin, l.cout, l.stride, bool(l.relu)) for l in wl.layers]
+    sub = [l.sub for l in wl.layers]
+    eng = _engine(wl.H, wl.W, wl.C0, layers, ws, sub, wl.dtype, wl.max_pillars)
+    strides = S.make_stream(name, n_strides=n_strides)
+    prev_bits = np.zeros((wl.H, wl.W, wl.C0), dtype=np.uint16 if wl.dtype == "bf16" else np.uint32)
+    prev_occ = np.zeros((wl.H, wl.W), bool)
+    for t, st in enumerate(strides):
+        note(f"[gpu-test] {name} stride {t} P={len(st.idx)}")
+        eng.step(*to_device(st, wl.dtype))
+        bits = canvas_bits(st, wl)
+        occ = SP.occupancy(st.idx, wl.H, wl.W)
+        check_lists(eng, SP.changed_lists(prev_bits, bits, prev_occ, occ, layers, sub), f"{name} stride {t}")
+        if t % map_every == 0 or t == len(strides) - 1:
+            x = oracle.exact_canvas(S.canvas(st, wl.H, wl.W, wl.C0), wl.dtype)
+            ys = SP.forward(x, occ, ws, layers, sub, bf16_storage=(wl.dtype == "bf16"))
+            check_maps(eng, ys, TOL[wl.dtype], f"{name} stride {t}")
+        prev_bits, prev_occ = bits, occ
+    eng.close()
+
+
+def test_s2_sparse_block1_100_strides():
+    _run("s2", 100, 25)
+
+
+def test_s3_sparse_backbone_40_strides():
+    _run("s3", 40, 10)
+
+
+def test_s4_sparse_backbone_bf16_40_strides():
+    _run("s4", 40, 20)
+
+
+STACKS = [
+    (19, 23, 32, [(32, 32, 1, True), (32, 32, 1, True), (32, 64, 2, True), (64, 64, 1, False)],
+     [False, True, False, True], "f32"),
+    (30, 17, 16, [(16, 16, 2, True), (16, 16, 1, True), (16, 8, 1, True)], [False, True, True], "f32"),
+    (25, 29, 64, [(64, 64, 2, True), (64, 128, 1, True), (128, 128, 1, True)], [False, False, True], "f32"),
+    (21, 18, 32, [(32, 32, 1, True), (32, 64, 2, True), (64, 64, 1, True)], [False, False, True], "bf16"),
+]
+
+
+@pytest.mark.parametrize("H,W,C0,layers,sub,dtype", STACKS)
+def test_random_sparse_stacks_with_toggles_and_zero_pillars(H, W, C0, layers, sub, dtype):
+    """Pillars appear and vanish every stride, some pillars carry all-zero
+    features (active sites holding zeros), the pillar order is shuffled."""
+    rng = np.random.default_rng(H * 100 + W)
+    ws = []
+    for (ci, co, _s, _r) in layers:
+        w = (rng.standard_normal((co, ci, 3, 3)) * np.sqrt(2.0 / (9 * ci))).astype(np.float32)
+        if dtype == "bf16":
+            w = S.bf16_bits_to_f32(S.round_to_bf16_bits(w)).reshape(w.shape)
+        ws.append(w)
+    eng = _engine(H, W, C0, layers, ws, sub, dtype, H * W)
+    occ = rng.random(H * W) < 0.2
+    feat = np.zeros((H * W, C0), np.float32)
+    feat[occ] = rng.standard_normal((int(occ.sum()), C0))
+    prev_bits, prev_occ = None, np.zeros((H, W), bool)
+    for t in range(20):
+        if t:
+            tog = rng.random(H * W) < 0.04
+            on = tog & ~occ
+            feat[tog & occ] = 0.0
+            feat[on] = rng.standard_normal((int(on.sum()), C0))
+            occ = occ ^ tog
+            r = occ & (rng.random(H * W) < 0.08)
+            feat[r] = rng.standard_normal((int(r.sum()), C0))
+        zero = occ & (rng.random(H * W) < 0.05)            # present pillars with all-zero features
+        feat[zero] = 0.0
+        idx = np.flatnonzero(occ).astype(np.int32)
+        idx = idx[rng.permutation(len(idx))]
+        f = feat[idx]
+        if dtype == "bf16":
+            fb = S.round_to_bf16_bits(f).reshape(f.shape)
+            feat[idx] = S.bf16_bits_to_f32(fb).reshape(f.shape)
+            st = S.Stride(t, idx, fb)
+        else:
+            st = S.Stride(t, idx, f.copy())
+        eng.step(*to_device(st, dtype))
+        canvas = S.canvas(st, H, W, C0)
+        bits = oracle.canvas_bits(canvas, dtype)
+        occ2 = occ.reshape(H, W).copy()
+        pb = np.zeros_like(bits) if prev_bits is None else prev_bits
+        check_lists(eng, SP.changed_lists(pb, bits, prev_occ, occ2, layers, sub), f"stride {t}")
+        x = oracle.exact_canvas(canvas, dtype)
+        check_maps(eng, SP.forward(x, occ2, ws, layers, sub, bf16_storage=(dtype == "bf16")), TOL[dtype],
+                   f"stride {t}")
+        prev_bits, prev_occ = bits, occ2
+    eng.reset()                                      # the active sets start over
+    eng.step(*to_device(st, dtype))
+    check_lists(eng, SP.changed_lists(np.zeros_like(bits), bits, np.zeros((H, W), bool), occ2, layers, sub),
+                "after reset")
+    check_maps(eng, SP.forward(x, occ2, ws, layers, sub, bf16_storage=(dtype == "bf16")), TOL[dtype], "after reset")
+    eng.close()
+
+
+def test_sparse_handle_refuses_dense_steps():
+    from paper_2512_08557_amd import SscaterError
+    wl = S.workload("s2")
+    eng = _engine(wl.H, wl.W, wl.C0, [(l.cin, l.cout, l.stride, bool(l.relu)) for l in wl.layers], S.weights("s2"),
+                  [l.sub for l in wl.layers], "f32", wl.max_pillars)
+    dense = torch.zeros((wl.H * wl.W, wl.C0), dtype=torch.float32, device="cuda")
+    with pytest.raises(SscaterError) as ei:
+        eng.step(None, dense)
+    assert ei.value.code == -1
+    eng.close()
