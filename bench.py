@@ -96,18 +96,28 @@ def cpu_baseline(wl, ws, strides, first, budget_s, neck=()):
     the neck when there is one, plus the change lists) on consecutive strides
     of the timed range, until the time budget is spent."""
     import oracle
+    from oracle import sparse as SP
     layers = layers_of(wl)
+    sub = [l.sub for l in wl.layers]
+    sparse = any(sub)
     ups = [(u.src, u.cout, u.stride, u.relu) for u in neck]
     uw = S.neck_weights(wl.name) if neck else []
     prev = oracle.canvas_bits(S.canvas(strides[first - 1], wl.H, wl.W, wl.C0), wl.dtype)
+    prev_occ = SP.occupancy(strides[first - 1].idx, wl.H, wl.W)
     t_total, u_total, n = 0.0, 0, 0
     for st in strides[first:]:
         canvas = S.canvas(st, wl.H, wl.W, wl.C0)
         t0 = time.perf_counter()
         bits = oracle.canvas_bits(canvas, wl.dtype)
         x = oracle.exact_canvas(canvas, wl.dtype)
-        ys = oracle.forward(x, ws, layers, bf16_storage=(wl.dtype == "bf16"))
-        lists = oracle.changed_lists(prev, bits, [l[2] for l in layers])
+        if sparse:
+            occ = SP.occupancy(st.idx, wl.H, wl.W)
+            ys = SP.forward(x, occ, ws, layers, sub, bf16_storage=(wl.dtype == "bf16"))
+            lists = SP.changed_lists(prev, bits, prev_occ, occ, layers, sub)
+            prev_occ = occ
+        else:
+            ys = oracle.forward(x, ws, layers, bf16_storage=(wl.dtype == "bf16"))
+            lists = oracle.changed_lists(prev, bits, [l[2] for l in layers])
         if ups:
             oracle.forward_neck(ys, uw, ups, bf16_storage=(wl.dtype == "bf16"))
         t_total += time.perf_counter() - t0
@@ -200,9 +210,9 @@ def short_kernel(name: str) -> str:
     fn, _, targs = base.partition("<")
     t = [x.strip() for x in targs.rstrip(">").split(",")]
     dt = lambda v: "bf16" if v == "true" else "f32"
-    if fn == "detect_kernel" and len(t) == 3:
+    if fn == "detect_kernel" and len(t) in (3, 4):
         return f"detect_kernel<{t[0]},{dt(t[1])},{'vanished' if t[2] == 'true' else 'present'}>"
-    if fn in ("layer_kernel", "layer_kernel_wide") and len(t) == 4:
+    if fn in ("layer_kernel", "layer_kernel_wide") and len(t) in (4, 5):
         return f"{fn}<{t[0]},{t[1]},{t[2]},{dt(t[3])}>"
     if fn == "pfn_kernel" and len(t) == 1:
         return f"pfn_kernel<{dt(t[0])}>"
@@ -484,9 +494,11 @@ def main() -> int:
         strides = S.make_stream(wl.name, n_strides=W + K)
         first = 1
         dev = upload(strides, wl.dtype)
+        sub = [l.sub for l in wl.layers]
         eng = Engine(wl.H, wl.W, wl.C0, layers_of(wl), ws, dtype=wl.dtype, max_pillars=wl.max_pillars,
                      ups=[(u.src, u.cout, u.stride, u.relu) for u in neck],
-                     up_weights=S.neck_weights(wl.name) if neck else ())
+                     up_weights=S.neck_weights(wl.name) if neck else (),
+                     submanifold=sub if any(sub) else None)
         step = lambda k: eng.step(*dev[k])
     L = len(wl.layers)
 
@@ -623,7 +635,9 @@ def main() -> int:
         "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.description}", "grid": f"{wl.W}x{wl.H}", "C0": wl.C0,
-                   "layers": [f"{l.cin}->{l.cout} s{l.stride}{' relu' if l.relu else ''}" for l in wl.layers],
+                   "layers": [f"{l.cin}->{l.cout} s{l.stride}{' relu' if l.relu else ''}"
+                              f"{' submanifold' if l.sub else (' sparse' if any(x.sub for x in wl.layers) else '')}"
+                              for l in wl.layers],
                    "neck": [f"up(layer {u.src}) {wl.layers[u.src - 1].cout}->{u.cout} x{u.stride}" for u in neck],
                    "strides": "full window + warmup untimed, then the timed delta strides",
                    **({"mean_points": float(np.mean([len(b) for b in strides[first + W:]])),
