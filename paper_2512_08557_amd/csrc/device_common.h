@@ -102,36 +102,48 @@ __device__ __forceinline__ bool memb_prev(uint64_t w, uint32_t epoch) {
     return (uint32_t)(w >> 33) == (epoch & 0x7FFFFFFFu) ? ((w >> 32) & 1ull) != 0ull : memb_now(w);
 }
 
-// Adds delta to the site's count; the first change of a stride records the
-// membership the site had before it.  Lock-free: a failed compare-and-swap
-// means another lane changed the word, and the loop retries on its value.
-__device__ __forceinline__ void memb_add(uint64_t* p, int delta, uint32_t epoch) {
-    const unsigned long long ep = epoch & 0x7FFFFFFFu;
-    unsigned long long old = __hip_atomic_load(reinterpret_cast<unsigned long long*>(p), __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT);
-    for (;;) {
-        const uint32_t cnt = (uint32_t)old;
-        const unsigned long long was = ((old >> 33) == ep) ? ((old >> 32) & 1ull) : (cnt != 0u ? 1ull : 0ull);
-        const unsigned long long nw = (ep << 33) | (was << 32) | (unsigned long long)(uint32_t)(cnt + (uint32_t)delta);
-        const unsigned long long got = atomicCAS(reinterpret_cast<unsigned long long*>(p), old, nw);
-        if (got == old) return;
-        old = got;
-    }
-}
-
 // Counts of the next regular layer: +-1 at every output site whose receptive
-// field holds `cell` (the same stride rule as the change lists).
+// field holds `cell` (the same stride rule as the change lists).  The targets'
+// words are loaded together and their compare-and-swaps issued together;
+// only a target that another lane changed in between goes round again.
 __device__ __forceinline__ void memb_spread(const MembTarget& t, int cell, int win, int delta, uint32_t epoch) {
+    const unsigned long long ep = epoch & 0x7FFFFFFFu;
     const int i = cell / win, j = cell - (cell / win) * win;
+    unsigned long long* ptr[9];
+    unsigned long long old[9];
+    bool todo[9];
+#pragma unroll
     for (int k = 0; k < 9; ++k) {
         int rn = i - k / 3 + 1, cn = j - k % 3 + 1;
+        bool ok = true;
         if (t.stride == 2) {
-            if ((rn | cn) & 1) continue;
+            ok = ((rn | cn) & 1) == 0;
             rn >>= 1;
             cn >>= 1;
         }
-        if (rn < 0 || rn >= t.Hout || cn < 0 || cn >= t.Wout) continue;
-        memb_add(t.memb + (size_t)rn * t.Wout + cn, delta, epoch);
+        ok = ok && rn >= 0 && rn < t.Hout && cn >= 0 && cn < t.Wout;
+        todo[k] = ok;
+        ptr[k] = reinterpret_cast<unsigned long long*>(t.memb) +
+                 (size_t)min(max(rn, 0), t.Hout - 1) * t.Wout + min(max(cn, 0), t.Wout - 1);
+        old[k] = ok ? __hip_atomic_load(ptr[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+    }
+    auto next_word = [&](unsigned long long w) {
+        const uint32_t cnt = (uint32_t)w;
+        const unsigned long long was = ((w >> 33) == ep) ? ((w >> 32) & 1ull) : (cnt != 0u ? 1ull : 0ull);
+        return (ep << 33) | (was << 32) | (unsigned long long)(uint32_t)(cnt + (uint32_t)delta);
+    };
+    unsigned long long got[9];
+#pragma unroll
+    for (int k = 0; k < 9; ++k) got[k] = todo[k] ? atomicCAS(ptr[k], old[k], next_word(old[k])) : 0ull;
+#pragma unroll
+    for (int k = 0; k < 9; ++k) {
+        if (!todo[k] || got[k] == old[k]) continue;
+        unsigned long long o = got[k];
+        for (;;) {
+            const unsigned long long g2 = atomicCAS(ptr[k], o, next_word(o));
+            if (g2 == o) break;
+            o = g2;
+        }
     }
 }
 
