@@ -238,7 +238,7 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
         // compiler drain every outstanding load where the branch joins.
         constexpr int NSTEP = 9 * NCH;
         constexpr int NSW = (NSTEP + KS - 1) / KS;
-        constexpr int PF = NCB == 1 ? 12 : (NCB == 2 ? 8 : 6);
+        constexpr int PF = NCB == 1 ? 9 : (NCB == 2 ? 8 : 6);
         int srow[NSW];
         bool sany[NSW];
 #pragma unroll
