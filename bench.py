@@ -169,7 +169,8 @@ def cpu_baseline_points(wl, ws, spec, pw, batches, first, budget_s):
 # HBM traffic of the dominant kernel from --pmc FETCH_SIZE / WRITE_SIZE runs
 # scaled by what the same counters read for a plain copy of known size.
 # --------------------------------------------------------------------------
-KERNEL_SOURCES = ("detect.hip", "layer.hip", "misc.hip", "device_common.h", "sscater_internal.h")
+KERNEL_SOURCES = ("detect.hip", "layer.hip", "misc.hip", "upsample.hip", "pfn.hip", "device_common.h",
+                  "sscater_internal.h")
 
 
 def kernel_source_digest() -> str:
@@ -184,22 +185,48 @@ def kernel_source_digest() -> str:
     return h.hexdigest()
 
 
-def read_traffic(kernel: str, workload: str):
-    """Measured HBM bytes per launch of `kernel`, or None when absent or stale."""
+def _traffic_records():
+    """The records of the traffic file: blocks of "key value" lines, each
+    opened by a "#" comment line."""
+    recs, cur = [], None
     try:
-        kv = {}
         with open(TRAFFIC_FILE) as fh:
             for line in fh:
-                line = line.strip()
-                if line and not line.startswith("#"):
-                    k, _, v = line.partition(" ")
-                    kv[k] = v.strip()
+                line = line.rstrip("\n")
+                if line.startswith("#"):
+                    cur = {"#": line}
+                    recs.append(cur)
+                elif line.strip() and cur is not None:
+                    k, _, v = line.strip().partition(" ")
+                    cur[k] = v.strip()
+    except OSError:
+        pass
+    return recs
+
+
+def read_traffic(kernel: str, workload: str):
+    """Measured HBM bytes per launch of `kernel` on `workload`, or None when
+    absent or stale (measured on other kernel sources)."""
+    for kv in _traffic_records():
         if (kv.get("source_sha256") == kernel_source_digest() and kv.get("kernel") == kernel
                 and kv.get("workload") == workload):
-            return float(kv["traffic_bytes_per_launch"])
-    except (OSError, KeyError, ValueError):
-        pass
+            try:
+                return float(kv["traffic_bytes_per_launch"])
+            except (KeyError, ValueError):
+                return None
     return None
+
+
+def write_traffic(rec: str, kernel: str, workload: str) -> None:
+    """Replace the record of (kernel, workload) in the traffic file by rec."""
+    keep = [r for r in _traffic_records() if not (r.get("kernel") == kernel and r.get("workload") == workload)]
+    out = []
+    for r in keep:
+        out.append(r["#"])
+        out += [f"{k} {v}" for k, v in r.items() if k != "#"]
+        out.append("")
+    with open(TRAFFIC_FILE, "w") as fh:
+        fh.write("\n".join(out) + rec)
 
 
 def short_kernel(name: str) -> str:
@@ -447,8 +474,7 @@ def main() -> int:
     if args.digest_pmc:
         per = launches_per_stride(args.kernel, S.workload(args.workload))
         rec = digest_pmc(*args.digest_pmc, args.copy_bytes, args.kernel, max(per, 1), args.steps, args.workload)
-        with open(TRAFFIC_FILE, "w") as fh:
-            fh.write(rec)
+        write_traffic(rec, args.kernel, args.workload)
         print(rec)
         return 0
     if args.copy_bytes:
