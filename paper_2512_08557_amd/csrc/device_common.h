@@ -147,6 +147,51 @@ __device__ __forceinline__ void memb_spread(const MembTarget& t, int cell, int w
     }
 }
 
+// prop_finish in two halves, so that the counter's round trip overlaps other
+// work: prop_reserve counts the owned targets and takes their list positions
+// (the atomic's result is not waited for), prop_write stores the entries.
+template <int G>
+struct PropSlots {
+    static constexpr int IT = PropBatch<G>::ITERS;
+    unsigned long long ob[IT];
+    bool own[IT];
+    int base, tot;
+};
+
+template <int G>
+__device__ __forceinline__ void prop_reserve(const PropTarget& t, uint32_t epoch, int shard, const PropBatch<G>& pb,
+                                             PropSlots<G>& ps) {
+    constexpr int IT = PropBatch<G>::ITERS;
+    int pairs = 0;
+    ps.tot = 0;
+    ps.base = 0;
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        ps.own[it] = pb.q[it] >= 0 && pb.old[it] < epoch;
+        pairs += (int)__popcll(__ballot(pb.q[it] >= 0));
+        ps.ob[it] = __ballot(ps.own[it]);
+        ps.tot += (int)__popcll(ps.ob[it]);
+    }
+    if (lane_id() == 0) {
+        if (ps.tot) ps.base = atomicAdd(t.count + shard * CSTRIDE, ps.tot);
+        if (pairs) atomicAdd(t.pairs + shard * CSTRIDE, pairs);
+    }
+}
+
+template <int G>
+__device__ __forceinline__ void prop_write(const PropTarget& t, int shard, const PropBatch<G>& pb, PropSlots<G>& ps) {
+    constexpr int IT = PropBatch<G>::ITERS;
+    if (ps.tot == 0) return;
+    const unsigned long long lt = (1ull << lane_id()) - 1ull;
+    int base = __shfl(ps.base, 0);
+    int32_t* seg = t.list + (size_t)shard * (t.Hout * t.Wout);
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+        if (ps.own[it]) seg[base + (int)__popcll(ps.ob[it] & lt)] = pb.q[it];
+        base += (int)__popcll(ps.ob[it]);
+    }
+}
+
 // fp32 -> bf16 bits, round to nearest even (finite values).
 __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
     uint32_t u = __float_as_uint(f);

@@ -420,6 +420,12 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
         // copies of the next tap overwrite the stage while the matrix cores
         // work; a small stage lets two workgroups share a compute unit, so
         // one computes while the other waits for its copies
+        // take the next layer's list positions now: the counter's round trip
+        // then overlaps the taps instead of ending the tile (measured on c3:
+        // 364 -> 355 us per stride; in the narrow kernel the same move stalls
+        // the first MFMAs on the footprint atomics and is slower)
+        PropSlots<4> ps;
+        if (do_prop) prop_reserve<4>(a.next, a.epoch, shard, pb, ps);
         f4v acc[1] = {f4v{0.f, 0.f, 0.f, 0.f}};
         if (taps) issue(__builtin_ctz(taps));
         while (taps) {
@@ -451,7 +457,7 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
             if (a.mnext.memb && h == 0 && cbl == 0 && g == 0 && vrow && now != prev)
                 memb_spread(a.mnext, q, a.Wout, now ? 1 : -1, a.epoch);
         }
-        if (do_prop) prop_finish<4>(a.next, a.epoch, shard, pb);
+        if (do_prop) prop_write<4>(a.next, shard, pb, ps);
         __syncthreads();                               // the stage buffers are free again
     }
     if (a.cum_dst && b == 0)
