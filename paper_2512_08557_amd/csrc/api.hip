@@ -7,7 +7,11 @@
 //   2. detect (vanished) : previous list minus the new list -> same outputs,
 //                          and the duplicate check of the new list;
 //   3. layer l = 1..L    : contraction over A_l, Z_l update, delta epilogue,
-//                          A_l -> A_{l+1} propagation.
+//                          A_l -> A_{l+1} propagation;
+//   4. the neck          : one upsampling launch per upsampler, when present.
+// Points mode replaces 1 and 2 by the pillar queue update and the pillar
+// feature net (sscater_step_points); a sparse backbone adds the active-set
+// words that detect and each block's first layer keep current.
 // Work sizes live in device counters; the layer kernels walk their tiles from
 // the counter, so the host never waits for a count.
 //

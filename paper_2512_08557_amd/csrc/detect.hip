@@ -13,6 +13,9 @@
 //              presence word (two pillars on one cell are an input fault).
 // The second pass needs the presence words of the whole first pass, so it is
 // a separate launch.
+// Sparse backbones (SPARSE): the pillar set is itself an input, so a pillar
+// that appeared or vanished is changed whatever its values, and it moves the
+// first layer's active-set counts (memb_spread).
 //
 // Layout: G = row_bytes / 16 lanes share one feature row, each lane moving 16
 // bytes, so a 64-channel fp32 row (256 B) is one fully coalesced 16-lane

@@ -38,6 +38,13 @@
 // Workgroup b walks the tiles of list segment (b / 8) % NSHARD; the
 // segments are filled by different workgroups of the previous launch so that
 // no single counter takes every append.
+//
+// Sparse backbones (SPARSE = true): a site inactive in this and in the
+// previous stride neither changes nor propagates; an inactive site's output is
+// zero in the delta epilogue; the first layer of a block passes its sites'
+// membership changes to the next block's active-set counts.  Z is updated at
+// every site of the list, active or not, so a site that joins the active set
+// already holds its sum.
 #include "device_common.h"
 
 #include <string.h>

@@ -83,7 +83,7 @@ static unsigned grid_for(long long n) {
     return (unsigned)b;
 }
 
-// n = element count, a multiple of 4 (channel counts are multiples of 16).
+// n = element count, a multiple of 4 (channel counts are multiples of 8).
 hipError_t launch_read(const float* Z, void* dst, long long n, int relu, bool bf16, hipStream_t s) {
     const long long n4 = n / 4;
     if (bf16) hipLaunchKernelGGL(read_kernel<true>, dim3(grid_for(n4)), dim3(256), 0, s, Z, dst, n4, relu);
@@ -103,7 +103,7 @@ hipError_t launch_read_masked(const float* Z, void* dst, long long cells, int co
     return hipGetLastError();
 }
 
-// ctot, coff and cout are multiples of 4 (channel counts are multiples of 16).
+// ctot, coff and cout are multiples of 4 (channel counts are multiples of 8).
 hipError_t launch_read_slice(const float* Z, void* dst, long long cells, int ctot, int coff, int cout, int relu,
                              bool bf16, hipStream_t s) {
     const long long n4 = cells * (cout / 4);
