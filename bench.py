@@ -624,6 +624,40 @@ def main() -> int:
                              "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
                                              "scaled by a plain copy)"})
 
+    # ---- floor: strides whose input equals the previous one bit for bit ----
+    # every launch of a stride runs and finds an empty list: the fixed cost of
+    # the stride's launch chain, beside the work-carrying strides above
+    floor = None
+    if not args.no_profile:
+        last_k = first + W + K - 1
+        nz = 20
+
+        def zero_change():
+            if spec is not None:
+                eng.step_points(None)      # no new points (the window keeps draining)
+            else:
+                step(last_k)
+
+        for _ in range(3):                 # settle
+            zero_change()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(nz):
+            zero_change()
+        torch.cuda.synchronize()
+        wall_floor = (time.perf_counter() - t0) / nz * 1e6
+        eng.profile_read()
+        eng.profile(True)
+        for _ in range(nz):
+            zero_change()
+        fms, fcnt = eng.profile_read()
+        eng.profile(False)
+        floor = {"stride_us": wall_floor,
+                 "kernels_us": {kernel_name(sl, wl, neck, points=spec is not None): fms[sl] / fcnt[sl] * 1e3
+                                for sl in range(len(fcnt)) if fcnt[sl]}}
+        log(f"[bench] zero-change stride: {floor['stride_us']:.1f} us; per launch "
+            + ", ".join(f"{k} {v:.2f} us" for k, v in floor["kernels_us"].items()))
+
     # ---- GPU full recompute: reset + full window through the same kernels ----
     full = []
     if spec is not None:       # every point of the last window in one step
@@ -678,6 +712,9 @@ def main() -> int:
         "alg_tflops": sum(2.0 * l.cin * l.cout * pairs[i + 1] for i, l in enumerate(wl.layers)) /
                       (wall_ms / 1e3) / 1e12,
         "full_recompute_ms": full_ms,
+        # the same launch chain on strides that change nothing (points mode:
+        # strides without new points, so only the expiring points change)
+        "zero_change_floor": floor,
         "speedup_vs_full_recompute": full_ms / ms_per_step if full_ms else None,
         "kernels": {n: {"launches": k["launches"], "avg_us": k["ms"] / k["launches"] * 1e3}
                     for n, k in kernels.items()},
