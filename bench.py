@@ -481,11 +481,11 @@ def main() -> int:
         return copy_calibration(args.copy_bytes)
 
     if args.gpus != 1:
-        log("bench.py: this build runs on one GPU only; multi-GPU runs are not supported "
+        log("bench.py: the benchmark runs on one GPU only; multi-GPU runs are not supported "
             "(independent sensor streams would shard one per GPU with no communication).")
         return 2
     if int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        log("bench.py: launched with WORLD_SIZE > 1; this build runs on one GPU only.")
+        log("bench.py: launched with WORLD_SIZE > 1; the benchmark runs on one GPU only.")
         return 2
 
     import torch
