@@ -182,6 +182,17 @@ int sscater_create_neck(const sscater_grid* grid, const sscater_layer* layers, i
                         const void* const* weights, const sscater_upsampler* ups, int32_t n_ups,
                         const void* const* up_weights, sscater_t* out);
 
+/* A handle over a batch of `batch` independent images of one grid (several
+ * sensor streams advanced together by one launch chain): as sscater_create,
+ * with cell index b * H * W + r * W + c for image b (pillar indices, change
+ * lists and maps alike; every map is [batch][H_l][W_l][C_l]); no convolution
+ * neighbourhood crosses an image boundary, so each image's results equal those
+ * of a handle of its own.  max_pillars bounds the pillars of all images
+ * together; H * W * batch at most 2^30.  No neck.  Errors as sscater_create,
+ * plus SSCATER_E_INVALID_ARG for batch < 1. */
+int sscater_create_batched(const sscater_grid* grid, int32_t batch, const sscater_layer* layers, int32_t n_layers,
+                           const void* const* weights, sscater_t* out);
+
 /* A handle in points mode (see sscater_pfn): layers and weights as for
  * sscater_create, C0 <= 64, pfn_weights the host [C0][9] fp32 weights of the
  * pointwise linear layer (copied).  Strides are then given as points with

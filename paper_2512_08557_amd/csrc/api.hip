@@ -78,6 +78,7 @@ struct sscater {
     int device = 0;
     sscater_grid grid{};
     int L = 0;
+    int batch = 1;                 // independent images of H x W cells each
     bool bf16 = false;
     int row_bytes = 0;      // bytes of one input feature row
     LayerState layers[SSCATER_MAX_LAYERS];
@@ -131,6 +132,10 @@ struct sscater {
     std::vector<ProfRec> prof_recs;
 
     int ncnt() const { return 2 * (L + 1) * NSHARD * CSTRIDE; }
+    // cells of layer l's output grid over the whole batch (l = 0: the input)
+    size_t cells_of(int l) const {
+        return (size_t)batch * (l == 0 ? (size_t)grid.H * grid.W : (size_t)layers[l - 1].Hout * layers[l - 1].Wout);
+    }
     int32_t* cnt_ptr(int set, int l) { return set_ptr(set) + (size_t)l * NSHARD * CSTRIDE; }
     int32_t* pairs_ptr(int set, int l) { return set_ptr(set) + (size_t)(L + 1 + l) * NSHARD * CSTRIDE; }
     int32_t* set_ptr(int s) { return counters + (size_t)s * ncnt(); }
@@ -213,6 +218,7 @@ PropTarget prop_target(sscater* h, int l /* consuming layer, 1..L */, int set) {
     t.Win = ls.Win;
     t.Hout = ls.Hout;
     t.Wout = ls.Wout;
+    t.seg = (int)h->cells_of(l);
     t.stamp = ls.stamp;
     t.list = ls.list;
     t.count = h->cnt_ptr(set, l);
@@ -229,7 +235,7 @@ int run_layers(sscater* h, int set, uint32_t epoch, hipStream_t s) {
         LayerArgs a{};
         a.list = ls.list;
         a.count = h->cnt_ptr(set, l);
-        a.cap = ls.Hout * ls.Wout;
+        a.cap = (int)h->cells_of(l);
         a.stamp_in = l == 1 ? h->stamp0 : h->layers[l - 2].stamp;
         a.delta_in = l == 1 ? h->delta0 : h->layers[l - 2].delta;
         a.wpack = ls.wpack;
@@ -311,11 +317,16 @@ int sscater_create(const sscater_grid* grid, const sscater_layer* layers, int32_
     return sscater_create_neck(grid, layers, n_layers, weights, nullptr, 0, nullptr, out);
 }
 
-int sscater_create_neck(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
-                        const void* const* weights, const sscater_upsampler* ups, int32_t n_ups,
-                        const void* const* up_weights, sscater_t* out) {
+}  // extern "C"
+
+namespace {
+
+int create_impl(const sscater_grid* grid, int32_t batch, const sscater_layer* layers, int32_t n_layers,
+                const void* const* weights, const sscater_upsampler* ups, int32_t n_ups,
+                const void* const* up_weights, sscater_t* out) {
     // ---- validation: host only, before any HIP call ----
     if (!grid || !layers || !weights || !out) return SSCATER_E_INVALID_ARG;
+    if (batch < 1 || (batch > 1 && n_ups > 0)) return SSCATER_E_INVALID_ARG;
     if (n_ups < 0 || n_ups > SSCATER_MAX_UPSAMPLERS || (n_ups > 0 && (!ups || !up_weights))) return SSCATER_E_INVALID_ARG;
     *out = nullptr;
     if (grid->H <= 0 || grid->W <= 0 || grid->C0 <= 0 || grid->max_pillars < 0) return SSCATER_E_INVALID_ARG;
@@ -323,7 +334,7 @@ int sscater_create_neck(const sscater_grid* grid, const sscater_layer* layers, i
     if (grid->dtype != SSCATER_F32 && grid->dtype != SSCATER_BF16) return SSCATER_E_INVALID_ARG;
     if (n_layers < 1 || n_layers > SSCATER_MAX_LAYERS) return SSCATER_E_INVALID_ARG;
     const bool bf16 = grid->dtype == SSCATER_BF16;
-    const long long cells0 = (long long)grid->H * grid->W;
+    const long long cells0 = (long long)grid->H * grid->W * batch;
     if (cells0 > (1LL << 30)) return SSCATER_E_INVALID_ARG;
     const int row_bytes = grid->C0 * (bf16 ? 2 : 4);
     if (!pow2(row_bytes) || row_bytes < 16 || row_bytes > 1024) return SSCATER_E_INVALID_ARG;
@@ -365,6 +376,7 @@ int sscater_create_neck(const sscater_grid* grid, const sscater_layer* layers, i
     sscater* h = new (std::nothrow) sscater();
     if (!h) return SSCATER_E_OUT_OF_MEMORY;
     h->grid = *grid;
+    h->batch = batch;
     h->L = n_layers;
     h->bf16 = bf16;
     h->row_bytes = row_bytes;
@@ -404,7 +416,7 @@ int sscater_create_neck(const sscater_grid* grid, const sscater_layer* layers, i
             ls.Win = W;
             ls.Hout = out_extent(H, ls.spec.stride);
             ls.Wout = out_extent(W, ls.spec.stride);
-            const size_t oc = (size_t)ls.Hout * ls.Wout;
+            const size_t oc = (size_t)batch * ls.Hout * ls.Wout;
             SSC_TRY(dev_alloc(h, (void**)&ls.Z, oc * ls.spec.cout * 4));
             SSC_TRY(dev_alloc(h, (void**)&ls.stamp, oc * 4));
             SSC_TRY(dev_alloc(h, (void**)&ls.list, oc * 4 * NSHARD));
@@ -461,10 +473,25 @@ fail:
     return rc;
 }
 
+}  // namespace
+
+extern "C" {
+
+int sscater_create_neck(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,
+                        const void* const* weights, const sscater_upsampler* ups, int32_t n_ups,
+                        const void* const* up_weights, sscater_t* out) {
+    return create_impl(grid, 1, layers, n_layers, weights, ups, n_ups, up_weights, out);
+}
+
+int sscater_create_batched(const sscater_grid* grid, int32_t batch, const sscater_layer* layers, int32_t n_layers,
+                           const void* const* weights, sscater_t* out) {
+    return create_impl(grid, batch, layers, n_layers, weights, nullptr, 0, nullptr, out);
+}
+
 int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
     if (!h || !pl || h->pfn) return SSCATER_E_INVALID_ARG;
     if (int rc = check_sticky(h)) return rc;
-    const long long cells = (long long)h->grid.H * h->grid.W;
+    const long long cells = (long long)h->cells_of(0);
     // NULL idx with count == H*W is dense mode; NULL idx with count 0 is an empty stride
     const bool dense = pl->idx == nullptr && pl->count != 0;
     if (dense && h->sparse) return SSCATER_E_INVALID_ARG;   // the pillar set is part of a sparse input
@@ -693,7 +720,7 @@ int sscater_create_sparse(const sscater_grid* grid, const sscater_layer* layers,
         ls.sub = submanifold[l] == 1;
         if (ls.sub) {
             ls.memb = h->layers[l - 1].memb;
-        } else if ((rc = dev_alloc(h, (void**)&ls.memb, (size_t)ls.Hout * ls.Wout * 8)) != SSCATER_OK) {
+        } else if ((rc = dev_alloc(h, (void**)&ls.memb, h->cells_of(l + 1) * 8)) != SSCATER_OK) {
             sscater_destroy(h);
             return rc;
         }
@@ -711,7 +738,7 @@ int sscater_read(sscater_t h, int32_t layer, void* dst, size_t dst_bytes, void* 
     hipStream_t s = static_cast<hipStream_t>(stream);
     const size_t esz = h->bf16 ? 2 : 4;
     if (layer == 0) {
-        const size_t need = (size_t)h->grid.H * h->grid.W * h->row_bytes;
+        const size_t need = h->cells_of(0) * h->row_bytes;
         if (dst_bytes < need) return SSCATER_E_INVALID_ARG;
         hipError_t e = hipMemcpyAsync(dst, h->X, need, hipMemcpyDeviceToDevice, s);
         return e == hipSuccess ? SSCATER_OK : hip_fail(e);
@@ -727,9 +754,9 @@ int sscater_read(sscater_t h, int32_t layer, void* dst, size_t dst_bytes, void* 
         return SSCATER_OK;
     }
     const LayerState& ls = h->layers[layer - 1];
-    const long long n = (long long)ls.Hout * ls.Wout * ls.spec.cout;
+    const long long n = (long long)h->cells_of(layer) * ls.spec.cout;
     if (dst_bytes < (size_t)n * esz) return SSCATER_E_INVALID_ARG;
-    hipError_t e = h->sparse ? launch_read_masked(ls.Z, dst, (long long)ls.Hout * ls.Wout, ls.spec.cout, ls.memb,
+    hipError_t e = h->sparse ? launch_read_masked(ls.Z, dst, (long long)h->cells_of(layer), ls.spec.cout, ls.memb,
                                                   ls.spec.relu, h->bf16, s)
                              : launch_read(ls.Z, dst, n, ls.spec.relu, h->bf16, s);
     return e == hipSuccess ? SSCATER_OK : hip_fail(e);
@@ -744,18 +771,18 @@ int sscater_reset(sscater_t h, void* stream) {
     // word, so a fault of a stride still in flight cannot survive the reset.
     hipError_t e = hipStreamSynchronize(s);
     if (e != hipSuccess) return hip_fail(e);
-    const size_t cells = (size_t)h->grid.H * h->grid.W;
+    const size_t cells = h->cells_of(0);
     e = launch_fill_zero(h->X, round_up(cells * h->row_bytes, 256), s);
     for (int l = 0; l < h->L && e == hipSuccess; ++l) {
         const LayerState& ls = h->layers[l];
-        e = launch_fill_zero(ls.Z, round_up((size_t)ls.Hout * ls.Wout * ls.spec.cout * 4, 256), s);
+        e = launch_fill_zero(ls.Z, round_up(h->cells_of(l + 1) * ls.spec.cout * 4, 256), s);
     }
     if (e == hipSuccess && h->Zn) e = launch_fill_zero(h->Zn, round_up((size_t)h->Hn * h->Wn * h->Cn * 4, 256), s);
     if (e == hipSuccess) e = launch_fill_zero(h->counters, round_up((size_t)2 * h->ncnt() * 4, 256), s);
     if (e == hipSuccess) e = launch_fill_zero(h->cum, round_up((size_t)h->ncnt() * 8, 256), s);
     for (int l = 0; l < h->L && e == hipSuccess && h->sparse; ++l) {
         const LayerState& ls = h->layers[l];
-        if (!ls.sub) e = launch_fill_zero(ls.memb, round_up((size_t)ls.Hout * ls.Wout * 8, 256), s);
+        if (!ls.sub) e = launch_fill_zero(ls.memb, round_up(h->cells_of(l + 1) * 8, 256), s);
     }
     if (e == hipSuccess && h->pfn) {
         const size_t slots = (size_t)h->pfn_spec.window + 1;
@@ -801,7 +828,7 @@ int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32
     std::vector<int32_t> buf;
     if (layer == 0 || layer == h->L + 1) {
         // A_0 and the neck's set: the cells stamped with the last stride's epoch
-        const int cells = layer == 0 ? h->grid.H * h->grid.W : h->Hn * h->Wn;
+        const int cells = layer == 0 ? (int)h->cells_of(0) : h->Hn * h->Wn;
         std::vector<uint32_t> st((size_t)cells);
         e = hipMemcpy(st.data(), layer == 0 ? h->stamp0 : h->stamp_n, st.size() * 4, hipMemcpyDeviceToHost);
         if (e != hipSuccess) return hip_fail(e);
@@ -813,7 +840,7 @@ int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32
         if (e != hipSuccess) return hip_fail(e);
         // the list segments; a segment never holds more entries than its grid has cells
         const LayerState& ls = h->layers[layer - 1];
-        const int cap_cells = ls.Hout * ls.Wout;
+        const int cap_cells = (int)h->cells_of(layer);
         for (int k = 0; k < NSHARD; ++k) {
             const int m = std::min(std::max(cnt[k * CSTRIDE], 0), cap_cells);
             if (m == 0) continue;
@@ -827,7 +854,7 @@ int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32
         // a sparse layer's changed sites: its work list minus the sites that
         // are active neither now nor in the previous stride
         const LayerState& ls = h->layers[layer - 1];
-        std::vector<uint64_t> mw((size_t)ls.Hout * ls.Wout);
+        std::vector<uint64_t> mw(h->cells_of(layer));
         e = hipMemcpy(mw.data(), ls.memb, mw.size() * 8, hipMemcpyDeviceToHost);
         if (e != hipSuccess) return hip_fail(e);
         const uint64_t ep = h->last_epoch & 0x7FFFFFFFu;

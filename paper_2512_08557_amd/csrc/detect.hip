@@ -117,7 +117,7 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
             *reinterpret_cast<uint4*>(xrow) = nv;
             if (sub == 0) a.stamp0[p] = a.epoch;
         }
-        if (SPARSE && tog && sub == 0) memb_spread(a.memb, p, a.next.Win, VANISH ? -1 : 1, a.epoch);
+        if (SPARSE && tog && sub == 0) memb_spread(a.memb, p, a.next.Hin, a.next.Win, VANISH ? -1 : 1, a.epoch);
         // |A_0|: one counter per shard, no returned value to wait for
         const int changed = (int)__popcll(__ballot(gd && sub == 0));
         if (lane == 0 && changed) atomicAdd(a.count0 + shard * CSTRIDE, changed);

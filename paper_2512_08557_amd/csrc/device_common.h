@@ -40,7 +40,9 @@ struct PropBatch {
 template <int G, bool UNCOND>
 __device__ __forceinline__ void prop_issue(const PropTarget& t, int cell, bool active, int sub, uint32_t epoch,
                                            PropBatch<G>& pb) {
-    const int i = cell / t.Win, j = cell - (cell / t.Win) * t.Win;
+    const int img = cell / (t.Hin * t.Win), loc = cell - img * (t.Hin * t.Win);
+    const int i = loc / t.Win, j = loc - (loc / t.Win) * t.Win;
+    const int obase = img * (t.Hout * t.Wout);
 #pragma unroll
     for (int it = 0; it < PropBatch<G>::ITERS; ++it) {
         const int k = sub + it * G;
@@ -53,7 +55,7 @@ __device__ __forceinline__ void prop_issue(const PropTarget& t, int cell, bool a
             cn >>= 1;
         }
         ok = ok && rn >= 0 && rn < t.Hout && cn >= 0 && cn < t.Wout;
-        const int q = min(max(rn, 0), t.Hout - 1) * t.Wout + min(max(cn, 0), t.Wout - 1);
+        const int q = obase + min(max(rn, 0), t.Hout - 1) * t.Wout + min(max(cn, 0), t.Wout - 1);
         pb.q[it] = ok ? q : -1;
         if (UNCOND) {
             pb.old[it] = atomicMax(&t.stamp[q], ok ? epoch : 0u);
@@ -87,7 +89,7 @@ __device__ __forceinline__ void prop_finish(const PropTarget& t, uint32_t epoch,
     }
     if (tot == 0) return;
     base = __shfl(base, 0);
-    int32_t* seg = t.list + (size_t)shard * (t.Hout * t.Wout);
+    int32_t* seg = t.list + (size_t)shard * t.seg;
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
         if (own[it]) seg[base + (int)__popcll(ob[it] & lt)] = pb.q[it];
@@ -106,9 +108,12 @@ __device__ __forceinline__ bool memb_prev(uint64_t w, uint32_t epoch) {
 // field holds `cell` (the same stride rule as the change lists).  The targets'
 // words are loaded together and their compare-and-swaps issued together;
 // only a target that another lane changed in between goes round again.
-__device__ __forceinline__ void memb_spread(const MembTarget& t, int cell, int win, int delta, uint32_t epoch) {
+__device__ __forceinline__ void memb_spread(const MembTarget& t, int cell, int hin, int win, int delta,
+                                            uint32_t epoch) {
     const unsigned long long ep = epoch & 0x7FFFFFFFu;
-    const int i = cell / win, j = cell - (cell / win) * win;
+    const int img = cell / (hin * win), loc = cell - img * (hin * win);
+    const int i = loc / win, j = loc - (loc / win) * win;
+    const size_t obase = (size_t)img * t.Hout * t.Wout;
     unsigned long long* ptr[9];
     unsigned long long old[9];
     bool todo[9];
@@ -123,7 +128,7 @@ __device__ __forceinline__ void memb_spread(const MembTarget& t, int cell, int w
         }
         ok = ok && rn >= 0 && rn < t.Hout && cn >= 0 && cn < t.Wout;
         todo[k] = ok;
-        ptr[k] = reinterpret_cast<unsigned long long*>(t.memb) +
+        ptr[k] = reinterpret_cast<unsigned long long*>(t.memb) + obase +
                  (size_t)min(max(rn, 0), t.Hout - 1) * t.Wout + min(max(cn, 0), t.Wout - 1);
         old[k] = ok ? __hip_atomic_load(ptr[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
     }
@@ -184,7 +189,7 @@ __device__ __forceinline__ void prop_write(const PropTarget& t, int shard, const
     if (ps.tot == 0) return;
     const unsigned long long lt = (1ull << lane_id()) - 1ull;
     int base = __shfl(ps.base, 0);
-    int32_t* seg = t.list + (size_t)shard * (t.Hout * t.Wout);
+    int32_t* seg = t.list + (size_t)shard * t.seg;
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
         if (ps.own[it]) seg[base + (int)__popcll(ps.ob[it] & lt)] = pb.q[it];

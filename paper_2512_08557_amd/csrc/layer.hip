@@ -172,7 +172,9 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
     while (tile * 16 < n) {
         const bool vrow = e < n;
         const int q = vrow ? qspec : 0;
-        const int qr = q / a.Wout, qc = q - (q / a.Wout) * a.Wout;
+        const int qimg = q / (a.Hout * a.Wout), ql = q - qimg * (a.Hout * a.Wout);
+        const int qr = ql / a.Wout, qc = ql - (ql / a.Wout) * a.Wout;
+        const int ibase = qimg * (a.Hin * a.Win);      // first cell of the input image
 
         // change stamps of the 9 input taps, all in flight together
         uint32_t ev[9];
@@ -182,7 +184,7 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
         for (int t = 0; t < 9; ++t) {
             const int ir = S * qr + t / 3 - 1, ic = S * qc + t % 3 - 1;
             inb[t] = vrow && ir >= 0 && ir < a.Hin && ic >= 0 && ic < a.Win;
-            cell[t] = min(max(ir, 0), a.Hin - 1) * a.Win + min(max(ic, 0), a.Win - 1);
+            cell[t] = ibase + min(max(ir, 0), a.Hin - 1) * a.Win + min(max(ic, 0), a.Win - 1);
             ev[t] = a.stamp_in[cell[t]];
         }
         float* zrow = a.Z + (size_t)q * COUT;
@@ -319,7 +321,7 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
         }
         if constexpr (SPARSE) {
             if (a.mnext.memb && wave == 0 && g == 0 && vrow && now != prev)
-                memb_spread(a.mnext, q, a.Wout, now ? 1 : -1, a.epoch);
+                memb_spread(a.mnext, q, a.Hout, a.Wout, now ? 1 : -1, a.epoch);
         }
         if (do_prop) prop_finish<4>(a.next, a.epoch, shard, pb);
 
@@ -381,14 +383,16 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
         const int e = (2 * pair + tp) * 16 + cl;
         const bool vrow = e < n;
         const int q = vrow ? seg[min(e, a.cap - 1)] : 0;
-        const int qr = q / a.Wout, qc = q - (q / a.Wout) * a.Wout;
+        const int qimg = q / (a.Hout * a.Wout), ql = q - qimg * (a.Hout * a.Wout);
+        const int qr = ql / a.Wout, qc = ql - (ql / a.Wout) * a.Wout;
+        const int ibase = qimg * (a.Hin * a.Win);
         int rows[9];
         unsigned mask = 0u;
 #pragma unroll
         for (int t = 0; t < 9; ++t) {
             const int ir = S * qr + t / 3 - 1, ic = S * qc + t % 3 - 1;
             const bool inb = vrow && ir >= 0 && ir < a.Hin && ic >= 0 && ic < a.Win;
-            const int cell = min(max(ir, 0), a.Hin - 1) * a.Win + min(max(ic, 0), a.Win - 1);
+            const int cell = ibase + min(max(ir, 0), a.Hin - 1) * a.Win + min(max(ic, 0), a.Win - 1);
             rows[t] = (inb && a.stamp_in[cell] == a.epoch) ? cell : -1;
             if (__ballot(rows[t] >= 0) != 0ull) mask |= 1u << t;
         }
@@ -462,7 +466,7 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
         if (vrow) epilogue4<COUT, BF16>(a, q, cbg * 16 + 4 * g, zo, acc[0], now, prev);
         if constexpr (SPARSE) {
             if (a.mnext.memb && h == 0 && cbl == 0 && g == 0 && vrow && now != prev)
-                memb_spread(a.mnext, q, a.Wout, now ? 1 : -1, a.epoch);
+                memb_spread(a.mnext, q, a.Hout, a.Wout, now ? 1 : -1, a.epoch);
         }
         if (do_prop) prop_write<4>(a.next, shard, pb, ps);
         __syncthreads();                               // the stage buffers are free again

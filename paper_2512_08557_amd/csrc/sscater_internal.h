@@ -23,10 +23,13 @@ constexpr int NSHARD = 2;
 constexpr int CSTRIDE = 32;
 
 // Change-list propagation target: the next layer's grid and its list state.
+// A handle may hold a batch of independent images: cell index
+// b * (H * W) + r * W + c; every neighbourhood stays inside its image.
 struct PropTarget {
     int stride;           // stride of the layer that consumes this list
-    int Hin, Win;         // grid the changed cells live in
-    int Hout, Wout;       // grid of the target list
+    int Hin, Win;         // image the changed cells live in
+    int Hout, Wout;       // image of the target list
+    int seg;              // cells of one list segment: batch * Hout * Wout
     uint32_t* stamp;      // [Hout*Wout]
     int32_t* list;        // NSHARD segments of Hout*Wout entries
     int32_t* count;       // segment lengths, segment k at count[k * CSTRIDE]

@@ -23,7 +23,8 @@ OK, E_INVALID_ARG, E_OUT_OF_MEMORY, E_HIP, E_OVERFLOW, E_DEVICE = 0, -1, -2, -3,
 F32, BF16 = 0, 1
 
 # every function declared in include/sscater.h
-EXPORTS = ("sscater_create", "sscater_create_neck", "sscater_create_pfn", "sscater_create_sparse", "sscater_step",
+EXPORTS = ("sscater_create", "sscater_create_neck", "sscater_create_pfn", "sscater_create_sparse",
+           "sscater_create_batched", "sscater_step",
            "sscater_step_points",
            "sscater_read", "sscater_reset", "sscater_destroy", "sscater_changed", "sscater_stats", "sscater_profile",
            "sscater_profile_read", "sscater_strerror")
@@ -88,6 +89,8 @@ def lib() -> ctypes.CDLL:
                                          ctypes.POINTER(ctypes.c_float), ctypes.POINTER(vp)]
         L.sscater_create_sparse.argtypes = [ctypes.POINTER(Grid), ctypes.POINTER(Layer), i32,
                                             ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(i32), ctypes.POINTER(vp)]
+        L.sscater_create_batched.argtypes = [ctypes.POINTER(Grid), i32, ctypes.POINTER(Layer), i32,
+                                             ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(vp)]
         L.sscater_step.argtypes = [vp, ctypes.POINTER(Pillars), vp]
         L.sscater_step_points.argtypes = [vp, vp, i32, vp]
         L.sscater_read.argtypes = [vp, i32, vp, ctypes.c_size_t, vp]
@@ -133,14 +136,17 @@ class Engine:
     def __init__(self, H: int, W: int, C0: int, layers: Sequence[Tuple[int, int, int, bool]],
                  weights: Sequence[np.ndarray], dtype: str = "f32", max_pillars: int = 16000,
                  ups: Sequence[Tuple[int, int, int, bool]] = (), up_weights: Sequence[np.ndarray] = (),
-                 pfn=None, pfn_weights: Optional[np.ndarray] = None, submanifold: Optional[Sequence[bool]] = None):
+                 pfn=None, pfn_weights: Optional[np.ndarray] = None, submanifold: Optional[Sequence[bool]] = None,
+                 batch: int = 1):
         """layers: (cin, cout, stride, relu); weights: OIHW per layer.  ups:
         optional neck, (src_layer, cout, stride, relu) per upsampler with
         [cin, cout, s, s] weights; the neck map is layer len(layers) + 1.
         pfn: optional points mode, (x_min, y_min, res, max_points, window,
         max_new_points) with [C0, 9] float32 pfn_weights; strides are then
         given to step_points.  submanifold: optional per-layer flags of a
-        sparse backbone (regular sparse layers where False)."""
+        sparse backbone (regular sparse layers where False).  batch: several
+        independent images of H x W in one handle (cell b*H*W + r*W + c);
+        read() then returns [batch, H, W, C]."""
         import torch  # device memory and streams only
         self._torch = torch
         self.H, self.W, self.C0 = H, W, C0
@@ -162,7 +168,13 @@ class Engine:
         self.ups = [tuple(u) for u in ups]
         self.pfn = tuple(pfn) if pfn is not None else None
         self.submanifold = [bool(x) for x in submanifold] if submanifold is not None else None
-        if self.submanifold is not None:
+        self.batch = int(batch)
+        if self.batch != 1:
+            if self.ups or self.pfn is not None or self.submanifold is not None:
+                raise ValueError("a batched handle takes no neck, points mode or sparse layers")
+            _check(lib().sscater_create_batched(ctypes.byref(grid), self.batch, larr, n, wptrs, ctypes.byref(handle)),
+                   "sscater_create_batched")
+        elif self.submanifold is not None:
             if self.ups or self.pfn is not None:
                 raise ValueError("a sparse backbone takes no neck and no points mode")
             if len(self.submanifold) != n:
@@ -219,7 +231,7 @@ class Engine:
                 raise ValueError("idx must be a contiguous int32 cuda tensor")
             count = idx.numel()
         else:
-            count = self.H * self.W
+            count = self.H * self.W * self.batch
         if count and (not feats.is_cuda or not feats.is_contiguous() or feats.element_size() !=
                       (4 if self.dtype == "f32" else 2) or feats.numel() != count * self.C0):
             raise ValueError("feats must be a contiguous cuda tensor [count, C0] of the grid dtype")
@@ -241,7 +253,8 @@ class Engine:
     def read(self, layer: int, out=None, stream=None):
         h, w, c = self.shapes[layer]
         if out is None:
-            out = self._torch.empty((h, w, c), dtype=self.torch_dtype, device="cuda")
+            shape = (h, w, c) if self.batch == 1 else (self.batch, h, w, c)
+            out = self._torch.empty(shape, dtype=self.torch_dtype, device="cuda")
         _check(lib().sscater_read(self._h, layer, ctypes.c_void_p(out.data_ptr()),
                                   out.numel() * out.element_size(), self._stream(stream)), "sscater_read")
         return out
@@ -251,7 +264,7 @@ class Engine:
 
     def changed(self, layer: int, stream=None) -> np.ndarray:
         h, w, _ = self.shapes[layer]
-        cap = h * w
+        cap = h * w * self.batch
         buf = np.empty(cap, dtype=np.int32)
         cnt = ctypes.c_int32(0)
         _check(lib().sscater_changed(self._h, layer, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), cap,

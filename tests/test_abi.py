@@ -229,3 +229,15 @@ def test_create_sparse_rejects_invalid_arguments(case):
     if rc == ssc.OK:
         lib.sscater_destroy(h)
     assert rc == ssc.E_INVALID_ARG
+
+
+@pytest.mark.parametrize("batch", [0, -1])
+def test_create_batched_rejects_invalid_batch(batch):
+    lib = ssc.lib()
+    g = E.Grid(16, 16, 64, 100, E.F32)
+    L = [E.Layer(64, 64, 3, 1, 1, 1)]
+    larr = (E.Layer * 1)(*L)
+    buf = np.zeros((64, 64, 3, 3), np.float32)
+    wp = (ctypes.c_void_p * 1)(buf.ctypes.data)
+    h = ctypes.c_void_p()
+    assert lib.sscater_create_batched(ctypes.byref(g), batch, larr, 1, wp, ctypes.byref(h)) == ssc.E_INVALID_ARG
