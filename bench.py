@@ -368,24 +368,40 @@ def copy_calibration(nbytes: int) -> int:
     return 0
 
 
-def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool) -> dict:
-    """n independent sensor streams (one handle each; scene seeds 2512 + k)
-    advanced together, each on its own HIP stream, as the 1024x1024
-    four-stream workload runs: whole-GPU throughput over K strides of every
-    stream, per-kernel timing from dispatch-stamped events on every handle."""
+def stack_strides(per_stream, H: int, W: int):
+    """One stride of a batched handle from one stride of every stream: image
+    b's pillar p becomes cell b*H*W + p."""
+    idx = np.concatenate([st.idx.astype(np.int64) + b * H * W for b, st in enumerate(per_stream)]).astype(np.int32)
+    feats = np.ascontiguousarray(np.concatenate([st.feats for st in per_stream]))
+    return S.Stride(per_stream[0].index, idx, feats)
+
+
+def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool, batched: bool = False) -> dict:
+    """n independent sensor streams (scene seeds 2512 + k) advanced together,
+    as the 1024x1024 four-stream workload runs: either one handle each on its
+    own HIP stream, or (batched) one handle over all n images, so that every
+    stride of all streams is one launch chain.  Whole-GPU throughput over K
+    strides of every stream, per-kernel timing from dispatch-stamped events
+    on every handle."""
     import torch
     from paper_2512_08557_amd import Engine
 
     data = [S.make_stream(wl.name, seed=S.SCENE_SEED + k, n_strides=W + K) for k in range(n)]
-    devs = [upload(st, wl.dtype) for st in data]
-    engs = [Engine(wl.H, wl.W, wl.C0, layers_of(wl), ws, dtype=wl.dtype, max_pillars=wl.max_pillars)
-            for _ in range(n)]
-    hs = [torch.cuda.Stream() for _ in range(n)]
+    if batched:
+        devs = [upload([stack_strides([d[k] for d in data], wl.H, wl.W) for k in range(len(data[0]))], wl.dtype)]
+        engs = [Engine(wl.H, wl.W, wl.C0, layers_of(wl), ws, dtype=wl.dtype, max_pillars=n * wl.max_pillars,
+                       batch=n)]
+        hs = [torch.cuda.Stream()]
+    else:
+        devs = [upload(st, wl.dtype) for st in data]
+        engs = [Engine(wl.H, wl.W, wl.C0, layers_of(wl), ws, dtype=wl.dtype, max_pillars=wl.max_pillars)
+                for _ in range(n)]
+        hs = [torch.cuda.Stream() for _ in range(n)]
     L = len(wl.layers)
 
     def run_range(lo, hi):
         for k in range(lo, hi):
-            for i in range(n):
+            for i in range(len(engs)):
                 engs[i].step(*devs[i][k], stream=hs[i])
 
     run_range(0, 1 + W)
@@ -400,8 +416,8 @@ def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool) -> di
     act = [[a["active_total"][l] - b["active_total"][l] for l in range(L + 1)] for a, b in zip(after, before)]
     updates = sum(sum(x[:L]) for x in act)
     value = updates / (wall_ms / 1e3)
-    log(f"[bench] {n} streams x {K} strides in {wall_ms:.2f} ms -> {wall_ms / K * 1e3:.1f} us per stride of all "
-        f"streams, {value:.3e} updates/s")
+    log(f"[bench] {n} streams ({'one batched handle' if batched else 'one handle each'}) x {K} strides in "
+        f"{wall_ms:.2f} ms -> {wall_ms / K * 1e3:.1f} us per stride of all streams, {value:.3e} updates/s")
 
     # per-kernel pass: the same strides again, every handle timed
     for e, h in zip(engs, hs):
@@ -437,7 +453,8 @@ def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool) -> di
                 "frac": achieved / PEAK_TFLOPS[wl.dtype], "traffic": read_traffic(dom_name, wl.name),
                 "kernel": dom_name, "launches": dom["launches"], "avg_launch_us": launch_us,
                 "alg_flops_per_launch": dom["flops"] / dom["launches"],
-                "note": "kernels of the different streams overlap; each duration is the kernel's own"}
+                "note": ("one launch per kernel and stride covers every stream" if batched else
+                         "kernels of the different streams overlap; each duration is the kernel's own")}
     for e in engs:
         e.close()
     cpu = None
@@ -451,7 +468,7 @@ def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool) -> di
             "ms_per_step": wall_ms / K, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
             "dtype": wl.dtype, "data": "synthetic",
             "config": {"workload": f"{wl.name}: {wl.description}", "grid": f"{wl.W}x{wl.H}", "C0": wl.C0,
-                       "streams": n, "layers": [f"{l.cin}->{l.cout} s{l.stride}" for l in wl.layers],
+                       "streams": n, "batched": batched, "layers": [f"{l.cin}->{l.cout} s{l.stride}" for l in wl.layers],
                        "strides": "a stride is one step of every stream; full window + warmup untimed",
                        "mean_active_per_stream": [sum(x[l] for x in act) / (K * n) for l in range(L + 1)]},
             "kernels": {k: {"launches": v["launches"], "avg_us": v["ms"] / v["launches"] * 1e3}
@@ -548,6 +565,8 @@ def main() -> int:
     ap.add_argument("--neck", action="store_true", help="include the upsampling neck (c3, c4)")
     ap.add_argument("--streams", type=int, default=0,
                     help="independent streams advanced together (default: 4 for c5, else 1)")
+    ap.add_argument("--separate", action="store_true",
+                    help="several streams: one handle per stream on its own HIP stream instead of one batched handle")
     ap.add_argument("--sweep", action="store_true",
                     help="single-layer channel sweep over all 20 (Cin, Cout) shapes on the 504x504 drone stream")
     ap.add_argument("--copy-bytes", type=int, default=0,
@@ -593,7 +612,8 @@ def main() -> int:
     K, W = args.steps, args.warmup
     n_streams = args.streams or (4 if wl.name == "c5" else 1)
     if n_streams > 1:
-        print(json.dumps(run_streams(wl, ws, K, W, n_streams, args.cpu_seconds, args.no_cpu)), flush=True)
+        print(json.dumps(run_streams(wl, ws, K, W, n_streams, args.cpu_seconds, args.no_cpu,
+                                     batched=not args.separate)), flush=True)
         return 0
     log(f"[bench] workload {wl.name}: {wl.description}; generating {W + K} delta strides")
     neck = S.neck(wl.name) if args.neck else ()
