@@ -354,6 +354,20 @@ def digest_pmc(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_bytes,
     return "\n".join(lines) + "\n"
 
 
+def digest_counters(path: str, kernel: str, per_stride: int, steps: int) -> str:
+    """Markdown table of every counter of a rocprofv3 --pmc csv, averaged over
+    the timed launches of `kernel` (its last steps*per_stride dispatches)."""
+    by = {}
+    for r in sorted(_csv_rows(path), key=lambda r: int(r["Dispatch_Id"])):
+        if short_kernel(r["Kernel_Name"]) == kernel:
+            by.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    out = [f"| Counter ({kernel}) | Dispatches | Mean per launch |", "|---|---|---|"]
+    for name in sorted(by):
+        v = by[name][-steps * per_stride:]
+        out.append(f"| {name} | {len(v)} | {statistics.fmean(v):.6g} |")
+    return "\n".join(out)
+
+
 def copy_calibration(nbytes: int) -> int:
     """A plain device-to-device copy of nbytes (the counters' calibration)."""
     import torch
@@ -574,7 +588,9 @@ def main() -> int:
     ap.add_argument("--digest-trace", metavar="CSV", help="summarise a rocprofv3 kernel-trace csv and exit")
     ap.add_argument("--digest-pmc", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
                     help="turn rocprofv3 --pmc csvs into the traffic record of the dominant kernel and exit")
-    ap.add_argument("--kernel", default="layer_kernel<64,64,1,f32>", help="kernel of --digest-pmc")
+    ap.add_argument("--digest-counters", metavar="CSV",
+                    help="average every counter of a rocprofv3 --pmc csv over the timed launches of --kernel and exit")
+    ap.add_argument("--kernel", default="layer_kernel<64,64,1,f32>", help="kernel of --digest-pmc / --digest-counters")
     args = ap.parse_args()
 
     if args.digest_trace:
@@ -582,6 +598,10 @@ def main() -> int:
             print(digest_sweep_trace(args.digest_trace, args.steps, args.warmup))
         else:
             print(digest_trace(args.digest_trace, args.steps, args.warmup, S.workload(args.workload)))
+        return 0
+    if args.digest_counters:
+        per = launches_per_stride(args.kernel, S.workload(args.workload))
+        print(digest_counters(args.digest_counters, args.kernel, max(per, 1), args.steps))
         return 0
     if args.digest_pmc:
         per = launches_per_stride(args.kernel, S.workload(args.workload))
