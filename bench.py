@@ -368,6 +368,53 @@ def digest_counters(path: str, kernel: str, per_stride: int, steps: int) -> str:
     return "\n".join(out)
 
 
+def copy_bandwidth(nbytes: int = 1 << 30, reps: int = 3) -> float:
+    """Measured HBM bandwidth of a plain device copy of nbytes (larger than
+    every cache): bytes read + written per second, best of reps, in GB/s."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    best = float("inf")
+    for _ in range(reps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        dst.copy_(src)
+        b.record()
+        torch.cuda.synchronize()
+        best = min(best, a.elapsed_time(b) / 1e3)
+    del src, dst
+    return 2.0 * nbytes / best / 1e9
+
+
+def stride_roofline(wl, act, pairs, K: int, mean_pillars: float, t_us: float, copy_gbs: float) -> dict:
+    """Roofline time of one stride from its algorithmic work, per layer the
+    larger of its flops at the MFMA peak and its bytes at the bandwidth, plus
+    the detection's bytes: t_roof = B_a1/BW + sum_l max(F_l/P, B_l/BW), against
+    the MI355X HBM peak and against the measured copy bandwidth; frac =
+    t_roof / the measured stride time.  act and pairs are per-layer totals
+    over the K timed strides."""
+    L = len(wl.layers)
+    bf16 = wl.dtype == "bf16"
+    e_in, e_d, e_w = (2.0 if bf16 else 4.0), 4.0, (2.0 if bf16 else 4.0)
+    peak = PEAK_TFLOPS[wl.dtype] * 1e12
+    A = [a / K for a in act]
+    P = mean_pillars
+    b_a1 = P * (4 + wl.C0 * e_in) + P * wl.C0 * e_in + A[0] * wl.C0 * (e_in + e_d) + 8.0 * P
+    fl, by = [], []
+    for l in range(1, L + 1):
+        sp = wl.layers[l - 1]
+        fl.append(2.0 * sp.cin * sp.cout * pairs[l] / K)
+        by.append(A[l - 1] * sp.cin * e_d + A[l] * sp.cout * 8.0 + (A[l] * sp.cout * e_d if l < L else 0.0) +
+                  9.0 * sp.cin * sp.cout * e_w + 8.0 * (A[l - 1] + A[l]))
+    out = {"t_measured_us": t_us, "alg_flops": sum(fl), "alg_bytes": b_a1 + sum(by), "copy_gbs": copy_gbs}
+    for tag, bw in (("spec", PEAK_HBM_GBS * 1e9), ("copy", copy_gbs * 1e9)):
+        t = b_a1 / bw + sum(max(f / peak, b / bw) for f, b in zip(fl, by))
+        out[f"t_roof_us_{tag}"] = t * 1e6
+        out[f"frac_{tag}"] = t * 1e6 / t_us
+    return out
+
+
 def copy_calibration(nbytes: int) -> int:
     """A plain device-to-device copy of nbytes (the counters' calibration)."""
     import torch
@@ -428,6 +475,7 @@ def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool, batch
     wall_ms = (time.perf_counter() - t0) * 1e3
     after = [e.stats(stream=h) for e, h in zip(engs, hs)]
     act = [[a["active_total"][l] - b["active_total"][l] for l in range(L + 1)] for a, b in zip(after, before)]
+    prs = [[a["pairs_total"][l] - b["pairs_total"][l] for l in range(L + 1)] for a, b in zip(after, before)]
     updates = sum(sum(x[:L]) for x in act)
     value = updates / (wall_ms / 1e3)
     log(f"[bench] {n} streams ({'one batched handle' if batched else 'one handle each'}) x {K} strides in "
@@ -471,6 +519,14 @@ def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool, batch
                          "kernels of the different streams overlap; each duration is the kernel's own")}
     for e in engs:
         e.close()
+    # all streams' work of one stride against the stride roofline
+    cgbs = copy_bandwidth()
+    sroof = stride_roofline(wl, [sum(x[l] for x in act) for l in range(L + 1)],
+                            [sum(x[l] for x in prs) for l in range(L + 1)], K,
+                            float(sum(np.mean([len(s.idx) for s in d[1 + W:]]) for d in data)), wall_ms / K * 1e3, cgbs)
+    log(f"[bench] stride roofline: {sroof['t_roof_us_spec']:.1f} us at 8 TB/s ({100 * sroof['frac_spec']:.1f} %), "
+        f"{sroof['t_roof_us_copy']:.1f} us at the measured copy bandwidth {cgbs:.0f} GB/s "
+        f"({100 * sroof['frac_copy']:.1f} %)")
     cpu = None
     if not no_cpu:
         try:
@@ -487,7 +543,7 @@ def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool, batch
                        "mean_active_per_stream": [sum(x[l] for x in act) / (K * n) for l in range(L + 1)]},
             "kernels": {k: {"launches": v["launches"], "avg_us": v["ms"] / v["launches"] * 1e3}
                         for k, v in kernels.items()},
-            "roofline": roofline, "cpu_baseline": cpu}
+            "roofline": roofline, "stride_roofline": sroof, "cpu_baseline": cpu}
 
 
 def run_sweep(K: int, W: int, n_full: int) -> dict:
@@ -815,6 +871,18 @@ def main() -> int:
     full_ms = statistics.median(full) if full else None
     eng.close()
 
+    # the whole stride against its own roofline (detection + every layer), for
+    # the pillar workloads; points mode adds the feature net, which this model
+    # does not price
+    sroof = None
+    if spec is None and not neck:
+        cgbs = copy_bandwidth()
+        sroof = stride_roofline(wl, act_in, pairs, K, float(np.mean([len(s.idx) for s in strides[1 + W:]])),
+                                ms_per_step * 1e3, cgbs)
+        log(f"[bench] stride roofline: {sroof['t_roof_us_spec']:.1f} us at 8 TB/s ({100 * sroof['frac_spec']:.1f} %), "
+            f"{sroof['t_roof_us_copy']:.1f} us at the measured copy bandwidth {cgbs:.0f} GB/s "
+            f"({100 * sroof['frac_copy']:.1f} %)")
+
     cpu = None
     if not args.no_cpu:
         try:
@@ -856,6 +924,7 @@ def main() -> int:
         "kernels": {n: {"launches": k["launches"], "avg_us": k["ms"] / k["launches"] * 1e3}
                     for n, k in kernels.items()},
         "roofline": roofline,
+        "stride_roofline": sroof,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
