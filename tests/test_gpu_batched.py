@@ -121,3 +121,63 @@ def test_random_batched_stacks_equal_separate_handles(H, W, C0, layers, dtype, B
         _compare(beng, sengs, len(layers), f"stride {t}")
     for e in sengs + [beng]:
         e.close()
+
+
+def test_batched_reset_empty_image_and_zero_change():
+    """A batch whose middle image never holds a pillar: its maps stay exactly
+    zero and its lists empty; a repeated stride changes nothing anywhere; after
+    reset the next stride is the full pass of every image again."""
+    rng = np.random.default_rng(77)
+    H, W, C0, B = 11, 13, 32, 3
+    layers = [(32, 32, 1, True), (32, 64, 2, True), (64, 64, 1, True)]
+    ws = [(rng.standard_normal((co, ci, 3, 3)) * np.sqrt(2.0 / (9 * ci))).astype(np.float32)
+          for (ci, co, _s, _r) in layers]
+    beng = _batched(H, W, C0, layers, ws, "f32", B, B * H * W)
+    seng = [make_engine_like(H, W, C0, layers, ws) for _ in (0, 2)]
+
+    def stride(t):
+        per = []
+        for b in (0, 2):
+            r = np.random.default_rng((t, b))
+            idx = np.flatnonzero(r.random(H * W) < 0.4).astype(np.int32)
+            per.append(S.Stride(t, idx, r.standard_normal((len(idx), C0)).astype(np.float32)))
+        return per
+
+    def run(t, per):
+        for e, st in zip(seng, per):
+            e.step(*to_device(st, "f32"))
+        empty = S.Stride(t, np.zeros(0, np.int32), np.zeros((0, C0), np.float32))
+        st = _stack([per[0], empty, per[1]], H, W)
+        beng.step(*to_device(st, "f32"))
+
+    def check(where):
+        for l in range(len(layers) + 1):
+            got = beng.read(l)
+            assert torch.equal(got[0], seng[0].read(l)), f"{where}: layer {l} image 0"
+            assert torch.equal(got[2], seng[1].read(l)), f"{where}: layer {l} image 2"
+            assert int(torch.count_nonzero(got[1])) == 0, f"{where}: layer {l} empty image not zero"
+            h, w, _c = seng[0].shapes[l]
+            ref = np.concatenate([seng[0].changed(l).astype(np.int64), seng[1].changed(l).astype(np.int64) + 2 * h * w])
+            np.testing.assert_array_equal(beng.changed(l), ref, err_msg=f"{where}: A_{l}")
+
+    for t in range(4):
+        per = stride(t)
+        run(t, per)
+        check(f"stride {t}")
+    before = [beng.read(l).clone() for l in range(len(layers) + 1)]
+    run(4, per)                                   # the same input again
+    for l in range(len(layers) + 1):
+        assert torch.equal(beng.read(l), before[l]), f"zero-change stride moved layer {l}"
+        assert len(beng.changed(l)) == 0, f"zero-change stride listed cells in A_{l}"
+    beng.reset()
+    for e in seng:
+        e.reset()
+    run(5, stride(5))
+    check("after reset")
+    for e in seng + [beng]:
+        e.close()
+
+
+def make_engine_like(H, W, C0, layers, ws):
+    from paper_2512_08557_amd import Engine
+    return Engine(H, W, C0, layers, ws, dtype="f32", max_pillars=H * W)
