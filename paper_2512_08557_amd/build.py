@@ -2,7 +2,8 @@
 
 Every HIP translation unit under csrc/ is compiled separately (in parallel)
 and linked into one shared library next to this file.  Packed-FP32 VALU
-instructions are disabled for all device code.
+instructions are disabled for all device code; the first five SGPRs of
+kernel arguments are preloaded (gfx950 kernarg preloading).
 """
 from __future__ import annotations
 
@@ -22,6 +23,9 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 COMMON = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # the layer kernels' leading (list, count, cap) arguments arrive in SGPRs,
+    # so their first loads need not wait for the kernel-argument fetch
+    "-mllvm", "-amdgpu-kernarg-preload-count=5",
     "-Wall", "-Wno-unused-result", "-I", os.path.join(ROOT, "include"),
 ]
 

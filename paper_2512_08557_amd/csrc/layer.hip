@@ -129,8 +129,13 @@ __device__ __forceinline__ void epilogue4(const LayerArgs& a, int q, int co0, co
     }
 }
 
+// plist, pcount, pcap are a.list, a.count, a.cap passed again as leading
+// scalar arguments: the build preloads them into SGPRs, so the list entry and
+// count loads that open every tile need not wait for the argument fetch.
 template <int CIN, int COUT, int S, bool BF16, bool SPARSE>
-__global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerArgs a) {
+__global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(const int32_t* __restrict__ plist,
+                                                                          const int32_t* __restrict__ pcount, int pcap,
+                                                                          LayerArgs a) {
     constexpr int NCBT = LayerShape<COUT>::NCBT;
     constexpr int NCB = LayerShape<COUT>::NCB;
     constexpr int NWC = LayerShape<COUT>::NWC, KS = LayerShape<COUT>::KS;
@@ -155,15 +160,15 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
     const int b = (int)blockIdx.x;
     const int shard = (b >> 3) % NSHARD;
     const int GS = G / NSHARD;                   // workgroups per segment
-    const int32_t* seg = a.list + (size_t)shard * a.cap;
+    const int32_t* seg = plist + (size_t)shard * pcap;
     const int hb = (b >> 3) / NSHARD;
     int tile = ((hb >> 2) << 5) + ((b & 7) << 2) + (hb & 3);
-    const int n = a.count[shard * CSTRIDE];
+    const int n = pcount[shard * CSTRIDE];
     int e = tile * 16 + cl;
     // loads are unconditional, from clamped (always valid) addresses, with the
     // result selected afterwards: a load inside a divergent branch makes the
     // compiler drain every outstanding load at the branch's end
-    int qspec = seg[min(e, a.cap - 1)];
+    int qspec = seg[min(e, pcap - 1)];
 
     if (a.cum_dst && b == 0)
         for (int i = (int)threadIdx.x; i < a.n_cum; i += (int)blockDim.x) a.cum_dst[i] += a.cum_src[i];
@@ -328,7 +333,7 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(LayerA
         tile += GS;
         e = tile * 16 + cl;
         if (tile * 16 >= n) break;
-        qspec = seg[min(e, a.cap - 1)];
+        qspec = seg[min(e, pcap - 1)];
     }
 }
 
@@ -356,8 +361,11 @@ struct WideShape {
     static constexpr int NH = NCBT / 2;                     // workgroups per tile pair
 };
 
+// plist, pcount, pcap: as for layer_kernel (preloaded copies of a.list,
+// a.count, a.cap).
 template <int CIN, int COUT, int S, bool BF16, bool SPARSE>
-__global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
+__global__ __launch_bounds__(256) void layer_kernel_wide(const int32_t* __restrict__ plist,
+                                                          const int32_t* __restrict__ pcount, int pcap, LayerArgs a) {
     using W = WideShape<CIN, COUT, BF16>;
     constexpr int NCH = W::NCH, NCBT = W::NCBT, NH = W::NH;
     constexpr int ROWB_IN = 4 * CIN;
@@ -372,8 +380,8 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
     const int h = b % NH;                              // cout blocks 2h, 2h+1
     const int shard = (b / NH) % NSHARD;
     const int GL = (int)gridDim.x / (NH * NSHARD);     // workgroups per (segment, cout group)
-    const int32_t* seg = a.list + (size_t)shard * a.cap;
-    const int n = a.count[shard * CSTRIDE];
+    const int32_t* seg = plist + (size_t)shard * pcap;
+    const int n = pcount[shard * CSTRIDE];
     const int cbg = 2 * h + cbl;                       // global cout block of this wavefront
     const bool do_prop = a.has_next && h == 0 && cbl == 0;
     const char* dbase = static_cast<const char*>(a.delta_in) + g * 16;
@@ -382,7 +390,7 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(LayerArgs a) {
     for (int pair = (b / NH) / NSHARD; pair * 32 < n; pair += GL) {
         const int e = (2 * pair + tp) * 16 + cl;
         const bool vrow = e < n;
-        const int q = vrow ? seg[min(e, a.cap - 1)] : 0;
+        const int q = vrow ? seg[min(e, pcap - 1)] : 0;
         const int qimg = q / (a.Hout * a.Wout), ql = q - qimg * (a.Hout * a.Wout);
         const int qr = ql / a.Wout, qc = ql - (ql / a.Wout) * a.Wout;
         const int ibase = qimg * (a.Hin * a.Win);
@@ -502,11 +510,13 @@ static hipError_t launch_shape(const LayerArgs& a, int grid, const LaunchCtx& c)
         constexpr int NH = WideShape<CI, CO, BF16>::NH;
         int gl = std::max(1, grid / (2 * NH * NSHARD));
         gl = std::min(gl, std::max(1, (a.cap + 31) / 32));
-        return launch_kernel(c, layer_kernel_wide<CI, CO, S, BF16, SPARSE>, dim3(gl * NH * NSHARD), dim3(256), a);
+        return launch_kernel(c, layer_kernel_wide<CI, CO, S, BF16, SPARSE>, dim3(gl * NH * NSHARD), dim3(256), a.list,
+                             a.count, a.cap, a);
     } else {
         // whole runs of 4 tiles on every XCD for every segment
         grid = std::max(32 * NSHARD, grid / (32 * NSHARD) * (32 * NSHARD));
-        return launch_kernel(c, layer_kernel<CI, CO, S, BF16, SPARSE>, dim3(grid), dim3(64 * LayerShape<CO>::NW), a);
+        return launch_kernel(c, layer_kernel<CI, CO, S, BF16, SPARSE>, dim3(grid), dim3(64 * LayerShape<CO>::NW), a.list,
+                             a.count, a.cap, a);
     }
 }
 

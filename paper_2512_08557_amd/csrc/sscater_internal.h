@@ -180,10 +180,10 @@ struct LaunchCtx {
     hipEvent_t start = nullptr, stop = nullptr;
 };
 
-template <class K, class A>
-inline hipError_t launch_kernel(const LaunchCtx& c, K kernel, dim3 grid, dim3 block, const A& args) {
-    if (c.start) hipExtLaunchKernelGGL(kernel, grid, block, 0, c.stream, c.start, c.stop, 0, args);
-    else hipLaunchKernelGGL(kernel, grid, block, 0, c.stream, args);
+template <class K, class... A>
+inline hipError_t launch_kernel(const LaunchCtx& c, K kernel, dim3 grid, dim3 block, const A&... args) {
+    if (c.start) hipExtLaunchKernelGGL(kernel, grid, block, 0, c.stream, c.start, c.stop, 0, args...);
+    else hipLaunchKernelGGL(kernel, grid, block, 0, c.stream, args...);
     return hipGetLastError();
 }
 
