@@ -173,12 +173,24 @@ KERNEL_SOURCES = ("detect.hip", "layer.hip", "misc.hip", "upsample.hip", "pfn.hi
                   "sscater_internal.h")
 
 
-def kernel_source_digest() -> str:
-    """sha256 over the device-code sources (not the host-side API): a measured
-    traffic figure is only reported while the kernels are the ones it was
-    measured on."""
+# the device-code sources each kernel family is built from
+KERNEL_FILES = {
+    "layer_kernel": ("layer.hip", "device_common.h", "sscater_internal.h"),
+    "detect_kernel": ("detect.hip", "device_common.h", "sscater_internal.h"),
+    "upsample_kernel": ("upsample.hip", "device_common.h", "sscater_internal.h"),
+    "pfn_kernel": ("pfn.hip", "device_common.h", "sscater_internal.h"),
+    "pillar_update_kernel": ("pfn.hip", "device_common.h", "sscater_internal.h"),
+}
+
+
+def kernel_source_digest(kernel: str = "") -> str:
+    """sha256 over the device-code sources `kernel` is built from (all of
+    them when the kernel is not named): a measured traffic figure is only
+    reported while the kernel is the one it was measured on."""
+    base = kernel.split("<")[0]
+    files = next((f for fam, f in KERNEL_FILES.items() if base == fam or base.startswith(fam + "_")), KERNEL_SOURCES)
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in files:
         h.update(name.encode())
         with open(os.path.join(ROOT, "paper_2512_08557_amd", "csrc", name), "rb") as fh:
             h.update(fh.read())
@@ -208,7 +220,7 @@ def read_traffic(kernel: str, workload: str):
     """Measured HBM bytes per launch of `kernel` on `workload`, or None when
     absent or stale (measured on other kernel sources)."""
     for kv in _traffic_records():
-        if (kv.get("source_sha256") == kernel_source_digest() and kv.get("kernel") == kernel
+        if (kv.get("source_sha256") == kernel_source_digest(kernel) and kv.get("kernel") == kernel
                 and kv.get("workload") == workload):
             try:
                 return float(kv["traffic_bytes_per_launch"])
@@ -338,7 +350,7 @@ def digest_pmc(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_bytes,
     traffic = fetch * 1024.0 * f_scale + write * 1024.0 * w_scale
     lines = [
         "# HBM traffic per launch of the dominant kernel (rocprofv3 --pmc FETCH_SIZE, WRITE_SIZE)",
-        f"source_sha256 {kernel_source_digest()}",
+        f"source_sha256 {kernel_source_digest(kernel)}",
         f"kernel {kernel}",
         f"workload {workload}",
         f"dispatches {len(fk)}",

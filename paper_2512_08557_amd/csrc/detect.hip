@@ -57,8 +57,10 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
             }
         }
         // presence: a pillar marks its cell present for this stride (plain
-        // store; the vanish pass checks ownership).  The canvas and feature
-        // rows are fetched in the same round trip as the presence word.
+        // store; the vanish pass checks ownership).  The present pass fetches
+        // the canvas and feature rows in the same round trip as the presence
+        // word; the vanish pass reads a canvas row only after the presence
+        // word showed the cell vanished.
         // Loads are unconditional from clamped addresses (selected afterwards):
         // a load inside a divergent branch makes the compiler drain all
         // outstanding loads where the branch ends.
@@ -80,17 +82,22 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
             a.pres[p] = mine;
         }
         char* xrow = static_cast<char*>(a.X) + (size_t)pc * ROWB + sub * 16;
-        uint4 ov = *reinterpret_cast<const uint4*>(xrow);
+        uint4 ov = make_uint4(0u, 0u, 0u, 0u);
         uint4 nv = make_uint4(0u, 0u, 0u, 0u);
-        if (!VANISH)
+        if (!VANISH) {
+            ov = *reinterpret_cast<const uint4*>(xrow);
             nv = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.feats) +
                                                  (size_t)min(i, a.count - 1) * ROWB + sub * 16);
-        if (VANISH) {
+        } else {
             act = act && st != a.epoch;                 // present in this stride: not vanished
             // every pillar of the new list must own its cell's presence word
             // (out-of-range cells were flagged by the present pass)
             if (a.chk_idx && sub == 0 && i < a.chk_count && c >= 0 && c < a.HW && cw != mine)
                 flag_error(a.err, ERR_DUPLICATE);
+            // only the canvas rows of vanished cells are read: most cells of
+            // the previous list are present again, and a wavefront without a
+            // vanished cell skips the load (a uniform branch)
+            if (__ballot(act) != 0ull) ov = *reinterpret_cast<const uint4*>(xrow);
         }
         bool tog = false;       // sparse backbones: the pillar appeared or vanished
         if (SPARSE) tog = VANISH ? act : (act && (op == 0ull || (uint32_t)(op >> 32) != a.epoch - 1u));
