@@ -824,6 +824,8 @@ def main() -> int:
                             "frac": achieved / PEAK_HBM_GBS, "traffic": traffic}
             roofline.update({"kernel": dom_name, "launches": dom["launches"],
                              "avg_launch_us": launch_us,
+                             # measured HBM bytes per launch over the launch time
+                             "traffic_gbs": traffic / (launch_us * 1e-6) / 1e9 if traffic else None,
                              "alg_flops_per_launch": dom["flops"] / dom["launches"],
                              "alg_bytes_per_launch": dom["bytes"] / dom["launches"],
                              "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
