@@ -380,6 +380,42 @@ def digest_counters(path: str, kernel: str, per_stride: int, steps: int) -> str:
     return "\n".join(out)
 
 
+def dense_torch_ms(wl, ws, canvases, reps: int = 20) -> float:
+    """Context: the same layer stack recomputed densely from the canvas by
+    the vendor convolution (torch conv2d, fp32 or bf16 storage as the
+    workload, NCHW, one image per canvas), ms per pass, median of reps."""
+    import torch
+    import torch.nn.functional as F
+    os.environ.setdefault("MIOPEN_FIND_MODE", "FAST")
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    x = torch.stack([torch.from_numpy(np.ascontiguousarray(
+        S.bf16_bits_to_f32(c.view(np.uint16)).reshape(c.shape) if wl.dtype == "bf16" else c)).permute(2, 0, 1)
+        for c in canvases]).contiguous().to("cuda", dt)
+    wt = [torch.from_numpy(np.ascontiguousarray(w)).to("cuda", dt) for w in ws]
+
+    def run():
+        y = x
+        for l, w in zip(wl.layers, wt):
+            y = F.conv2d(y, w, stride=l.stride, padding=1)
+            if l.relu:
+                y = torch.relu(y)
+        return y
+
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        run()
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    return statistics.median(times)
+
+
 def copy_bandwidth(nbytes: int = 1 << 30, reps: int = 3) -> float:
     """Measured HBM bandwidth of a plain device copy of nbytes (larger than
     every cache): bytes read + written per second, best of reps, in GB/s."""
@@ -449,7 +485,8 @@ def stack_strides(per_stream, H: int, W: int):
     return S.Stride(per_stream[0].index, idx, feats)
 
 
-def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool, batched: bool = False) -> dict:
+def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool, batched: bool = False,
+                dense: bool = False) -> dict:
     """n independent sensor streams (scene seeds 2512 + k) advanced together,
     as the 1024x1024 four-stream workload runs: either one handle each on its
     own HIP stream, or (batched) one handle over all n images, so that every
@@ -531,6 +568,11 @@ def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool, batch
                          "kernels of the different streams overlap; each duration is the kernel's own")}
     for e in engs:
         e.close()
+    dense_ms = None
+    if dense:      # context: the vendor library's dense recompute of every stream (a batch of n images)
+        dense_ms = dense_torch_ms(wl, ws, [S.canvas(d[W + K], wl.H, wl.W, wl.C0) for d in data])
+        log(f"[bench] dense recompute with torch conv2d: {dense_ms * 1e3:.1f} us per pass of all streams "
+            f"({dense_ms / (wall_ms / K):.1f}x the delta stride)")
     # all streams' work of one stride against the stride roofline
     cgbs = copy_bandwidth()
     sroof = stride_roofline(wl, [sum(x[l] for x in act) for l in range(L + 1)],
@@ -555,7 +597,7 @@ def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool, batch
                        "mean_active_per_stream": [sum(x[l] for x in act) / (K * n) for l in range(L + 1)]},
             "kernels": {k: {"launches": v["launches"], "avg_us": v["ms"] / v["launches"] * 1e3}
                         for k, v in kernels.items()},
-            "roofline": roofline, "stride_roofline": sroof, "cpu_baseline": cpu}
+            "dense_torch_ms": dense_ms, "roofline": roofline, "stride_roofline": sroof, "cpu_baseline": cpu}
 
 
 def run_sweep(K: int, W: int, n_full: int) -> dict:
@@ -644,6 +686,8 @@ def main() -> int:
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-kernel event pass")
     ap.add_argument("--no-full", action="store_true", help="skip the GPU full-recompute timing")
+    ap.add_argument("--dense-torch", action="store_true",
+                    help="context: time the same layers recomputed densely by torch conv2d (the vendor library)")
     ap.add_argument("--neck", action="store_true", help="include the upsampling neck (c3, c4)")
     ap.add_argument("--streams", type=int, default=0,
                     help="independent streams advanced together (default: 4 for c5, else 1)")
@@ -701,7 +745,7 @@ def main() -> int:
     n_streams = args.streams or (4 if wl.name == "c5" else 1)
     if n_streams > 1:
         print(json.dumps(run_streams(wl, ws, K, W, n_streams, args.cpu_seconds, args.no_cpu,
-                                     batched=not args.separate)), flush=True)
+                                     batched=not args.separate, dense=args.dense_torch)), flush=True)
         return 0
     log(f"[bench] workload {wl.name}: {wl.description}; generating {W + K} delta strides")
     neck = S.neck(wl.name) if args.neck else ()
@@ -885,6 +929,13 @@ def main() -> int:
     full_ms = statistics.median(full) if full else None
     eng.close()
 
+    # context: the vendor library's dense recompute of the same layers
+    dense_ms = None
+    if args.dense_torch and spec is None and not neck and not any(l.sub for l in wl.layers):
+        dense_ms = dense_torch_ms(wl, ws, [S.canvas(strides[W + K], wl.H, wl.W, wl.C0)])
+        log(f"[bench] dense recompute with torch conv2d: {dense_ms * 1e3:.1f} us per pass "
+            f"({dense_ms / ms_per_step:.1f}x the delta stride)")
+
     # the whole stride against its own roofline (detection + every layer), for
     # the pillar workloads; points mode adds the feature net, which this model
     # does not price
@@ -931,6 +982,7 @@ def main() -> int:
         "alg_tflops": sum(2.0 * l.cin * l.cout * pairs[i + 1] for i, l in enumerate(wl.layers)) /
                       (wall_ms / 1e3) / 1e12,
         "full_recompute_ms": full_ms,
+        "dense_torch_ms": dense_ms,
         # the same launch chain on strides that change nothing (points mode:
         # strides without new points, so only the expiring points change)
         "zero_change_floor": floor,
