@@ -231,10 +231,12 @@ def test_create_sparse_rejects_invalid_arguments(case):
     assert rc == ssc.E_INVALID_ARG
 
 
-@pytest.mark.parametrize("batch", [0, -1])
-def test_create_batched_rejects_invalid_batch(batch):
+@pytest.mark.parametrize("batch,hw", [(0, 16), (-1, 16), (1 << 11, 1 << 10)])
+def test_create_batched_rejects_invalid_batch(batch, hw):
+    """batch < 1, and a batch whose cells exceed 2^30 (host-side checks made
+    before any HIP call)."""
     lib = ssc.lib()
-    g = E.Grid(16, 16, 64, 100, E.F32)
+    g = E.Grid(hw, hw, 64, 100, E.F32)
     L = [E.Layer(64, 64, 3, 1, 1, 1)]
     larr = (E.Layer * 1)(*L)
     buf = np.zeros((64, 64, 3, 3), np.float32)
