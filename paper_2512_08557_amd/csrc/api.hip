@@ -380,6 +380,11 @@ int create_impl(const sscater_grid* grid, int32_t batch, const sscater_layer* la
     h->L = n_layers;
     h->bf16 = bf16;
     h->row_bytes = row_bytes;
+    // layer launches: 1024 workgroups per image, at most 4096 (a batch of
+    // images carries that many more tiles per launch; measured on four
+    // 1024x1024 images: 4096 workgroups 196 us per stride against 202 us
+    // with 1024); SSCATER_LAYER_GRID overrides it
+    h->layer_grid = (int)std::min<long long>(4096, 1024LL * batch);
     if (const char* g = getenv("SSCATER_LAYER_GRID")) {
         const int v = atoi(g);
         if (v >= 32 && v <= 65536) h->layer_grid = v & ~31;
