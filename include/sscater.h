@@ -241,7 +241,10 @@ int sscater_create_sparse(const sscater_grid* grid, const sscater_layer* layers,
  * nothing.  Asynchronous on `stream`. */
 int sscater_step(sscater_t h, const sscater_pillars* pillars, void* stream);
 
-/* Write layer `layer`'s output map into dst (device, NHWC, grid dtype):
+/* Write layer `layer`'s output map into dst (device, NHWC, grid dtype): the
+ * maps the method keeps between passes and updates in place (Sec. III-D: the
+ * previous output is kept and only the delta contributions are added; the
+ * abstract and Sec. IV-G: the kept maps equal recomputation).
  * layer 0 = the input canvas, layer l = 1..L = phi(Z_l) (bf16-rounded for the
  * bf16 dtype), layer L + 1 = the neck map (each upsampler's phi over its
  * channels) when the handle has a neck.  dst_bytes must be at least
@@ -249,23 +252,39 @@ int sscater_step(sscater_t h, const sscater_pillars* pillars, void* stream);
 int sscater_read(sscater_t h, int32_t layer, void* dst, size_t dst_bytes, void* stream);
 
 /* Return to the empty window: zero the canvas and maps, forget the change
- * lists and clear the sticky device error.  Asynchronous on `stream`. */
+ * lists and clear the sticky device error, so the next step is again the
+ * initial full pass of Alg. 1 (the first window is built from nothing before
+ * the strides start; Sec. III-B).  The stream is synchronised first, so a
+ * device fault of a stride still in flight cannot outlive the reset; the
+ * clears themselves are enqueued on `stream`. */
 int sscater_reset(sscater_t h, void* stream);
 
 /* Free everything.  The caller must make sure no work of the handle is still
  * pending on any stream. */
 int sscater_destroy(sscater_t h);
 
-/* Test / metrics extension: the last stride's change list A_layer
- * (0 <= layer <= L, or L + 1 for the neck) sorted row-major into the HOST
- * buffer dst[cap]; the list
- * length goes to *count_host (also when it exceeds cap, in which case only cap
- * entries are written).  Synchronises `stream`. */
+/* Test / metrics extension: the last stride's change map of layer `layer`
+ * (Alg. 1: the per-layer map of sites changed by the convolution or the
+ * ReLU, and for stride 2 the downsampled sites under a changed site) as a
+ * list of cell indices A_layer (0 <= layer <= L, or L + 1 for the neck),
+ * sorted row-major into the HOST buffer dst[cap].  dst is host memory, not
+ * device memory: the call exists for tests and metrics, it must sort the
+ * device's unordered list segments, and every caller reads the result on
+ * the host, so it synchronises `stream`, copies the segments down and sorts
+ * there.  The list length goes to *count_host (also when it exceeds cap, in
+ * which case only cap entries are written).  Errors: SSCATER_E_INVALID_ARG
+ * for a null handle or count_host, a layer out of range, cap < 0 or a null
+ * dst with cap > 0; SSCATER_E_DEVICE when the sticky flag is set. */
 int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32_t* count_host,
                     void* stream);
 
-/* Test / metrics extension: counters of the last stride and totals.
- * Synchronises `stream`. */
+/* Test / metrics extension: counters of the last stride and totals into the
+ * host struct *out: |A_l| per layer (the sizes of Alg. 1's change maps), the
+ * (changed input, in-grid tap) pairs each layer contracted (Eq. 2's scatter
+ * terms; 2 * cin * cout flops each), and the stride's algorithmic flops and
+ * HBM bytes.  Synchronises `stream`.  Errors: SSCATER_E_INVALID_ARG for a
+ * null handle or out; SSCATER_E_DEVICE when the sticky flag is set (the
+ * counters are still written). */
 int sscater_stats(sscater_t h, sscater_stats_t* out, void* stream);
 
 /* Metrics extension: per-kernel timing of every launch of sscater_step (and

@@ -212,9 +212,20 @@ class Engine:
         self._wbufs = None   # copied by the library
 
     # -- helpers ---------------------------------------------------------------
-    def _stream(self, stream=None) -> ctypes.c_void_p:
+    def _stream(self, stream=None, tensors=()) -> ctypes.c_void_p:
+        """The HIP stream handle of a call.  A stream other than the current
+        one first waits for the current stream (where the caller's tensors
+        were produced), and every tensor the call reads or writes is recorded
+        on it, so the caching allocator does not hand the memory out again
+        before the library's kernels on that stream are done with it."""
         t = self._torch
-        s = stream if stream is not None else t.cuda.current_stream()
+        cur = t.cuda.current_stream()
+        s = stream if stream is not None else cur
+        if s != cur:
+            s.wait_stream(cur)
+            for x in tensors:
+                if x is not None:
+                    x.record_stream(s)
         return ctypes.c_void_p(s.cuda_stream)
 
     @property
@@ -236,7 +247,8 @@ class Engine:
                       (4 if self.dtype == "f32" else 2) or feats.numel() != count * self.C0):
             raise ValueError("feats must be a contiguous cuda tensor [count, C0] of the grid dtype")
         p = Pillars(idx.data_ptr() if idx is not None else None, feats.data_ptr() if count else None, count)
-        _check(lib().sscater_step(self._h, ctypes.byref(p), self._stream(stream)), "sscater_step")
+        _check(lib().sscater_step(self._h, ctypes.byref(p), self._stream(stream, (idx, feats if count else None))),
+               "sscater_step")
 
     def step_points(self, points, stream=None) -> None:
         """points: contiguous float32 cuda tensor [n, 4] = (x, y, z, intensity)
@@ -248,7 +260,8 @@ class Engine:
                 raise ValueError("points must be a contiguous float32 cuda tensor [n, 4]")
             n = points.shape[0]
         ptr = ctypes.c_void_p(points.data_ptr() if n else None)
-        _check(lib().sscater_step_points(self._h, ptr, n, self._stream(stream)), "sscater_step_points")
+        _check(lib().sscater_step_points(self._h, ptr, n, self._stream(stream, (points if n else None,))),
+               "sscater_step_points")
 
     def read(self, layer: int, out=None, stream=None):
         h, w, c = self.shapes[layer]
@@ -256,7 +269,7 @@ class Engine:
             shape = (h, w, c) if self.batch == 1 else (self.batch, h, w, c)
             out = self._torch.empty(shape, dtype=self.torch_dtype, device="cuda")
         _check(lib().sscater_read(self._h, layer, ctypes.c_void_p(out.data_ptr()),
-                                  out.numel() * out.element_size(), self._stream(stream)), "sscater_read")
+                                  out.numel() * out.element_size(), self._stream(stream, (out,))), "sscater_read")
         return out
 
     def reset(self, stream=None) -> None:

@@ -59,15 +59,18 @@ def map_errors(eng, ys_ref):
 
 
 def check_maps(eng, ys_ref, tol, where="", floors=None):
-    """max|gpu - ref| <= tol * max|ref| per layer.  floors: optional per-layer
-    scale to use instead when it is larger (the largest max|ref| the layer held
-    earlier in the run: once a window drains to zero, recycled maps keep the
-    rounding residue of the deltas that cancelled, which only that earlier
-    scale measures)."""
+    """max|gpu - ref| <= tol * max|ref| per layer, with that stride's max|ref|.
+    A layer whose reference is all zero must read zero up to 1e-6 absolute;
+    floors (optional, per layer) replaces that bar for such a layer only, by
+    tol times the largest max|ref| the layer held earlier in the run: a window
+    that drained to nothing leaves the rounding residue of the deltas that
+    cancelled in the recycled fp32 maps, and only that earlier scale measures
+    it."""
     for l, (err, scale) in enumerate(map_errors(eng, ys_ref), start=1):
-        if floors is not None:
-            scale = max(scale, floors[l - 1])
-        if scale == 0.0:
+        if scale == 0.0 and floors is not None and floors[l - 1] > 0.0:
+            assert err <= tol * floors[l - 1], \
+                f"{where} layer {l}: drained reference, max|gpu| {err:.3e} > {tol} * {floors[l - 1]:.3e}"
+        elif scale == 0.0:
             assert err <= 1e-6, f"{where} layer {l}: reference is zero, max|gpu| = {err}"
         else:
             assert err <= tol * scale, f"{where} layer {l}: max err {err:.3e} > {tol} * {scale:.3e}"

@@ -110,3 +110,110 @@ def test_change_lists_cover_every_value_change_and_stay_in_the_active_sets():
 def test_submanifold_requires_stride_one():
     with pytest.raises(AssertionError):
         SP.active_sets(np.ones((4, 4), bool), [(1, 1, 2, True)], [True])
+
+
+def _value_changed_lists(ys_a, ys_b, x_a, x_b):
+    """Cells whose value differs between two windows, per layer (layer 0 the
+    canvas): the value semantics the change sets must reproduce."""
+    out = [np.flatnonzero(np.any(x_a != x_b, axis=-1))]
+    for a, b in zip(ys_a, ys_b):
+        out.append(np.flatnonzero(np.any(a != b, axis=-1)))
+    return out
+
+
+def _unmasked_variant(prev_bits, new_bits, prev_occ, new_occ, layers, sub):
+    """A plausible misreading kept here only to show the pin rejects it: the
+    receptive-field rule propagates the unmasked set, and only each layer's
+    reported set is restricted to the active sites."""
+    m = np.any(prev_bits != new_bits, axis=-1) | (prev_occ ^ new_occ)
+    out = [np.flatnonzero(m)]
+    s_old, s_new = SP.active_sets(prev_occ, layers, sub), SP.active_sets(new_occ, layers, sub)
+    for (_ci, _co, stride, _r), so, sn in zip(layers, s_old, s_new):
+        m = oracle.propagate_gather(m, stride)
+        out.append(np.flatnonzero(m & (so | sn)))
+    return out
+
+
+def _lists_of(x_a, x_b, occ_a, occ_b, layers, sub, fn=SP.changed_lists):
+    return fn(oracle.canvas_bits(x_a.astype(np.float32), "f32"), oracle.canvas_bits(x_b.astype(np.float32), "f32"),
+              occ_a, occ_b, layers, sub)
+
+
+def test_worked_example_change_sets_stop_at_inactive_sites():
+    """Pillars at (2, 2) and (2, 6) of a 5 x 9 grid, one channel, all-ones
+    weights, no ReLU; a regular stride-1 layer and two submanifold layers.
+    The regular layer's active set is the two 3 x 3 blocks (columns 1-3 and
+    5-7); column 4 is empty in both windows.  Refreshing the pillar at (2, 2)
+    changes the 3 x 3 block around it in layer 1, and the submanifold layers
+    cannot leave their active set, so layers 2 and 3 change exactly the same
+    block: rows 1-3, columns 1-3.  Propagating through the empty column 4
+    (reading the rule without the restriction) would also mark rows 1-3 of
+    column 5 in layer 3, whose values do not move."""
+    x = np.zeros((5, 9, 1))
+    occ = np.zeros((5, 9), bool)
+    for c in (2, 6):
+        occ[2, c] = True
+        x[2, c, 0] = 1.0
+    x2 = x.copy()
+    x2[2, 2, 0] = 2.0
+    layers = [(1, 1, 1, False)] * 3
+    sub = [False, True, True]
+    block = sorted(r * 9 + c for r in (1, 2, 3) for c in (1, 2, 3))
+    lists = _lists_of(x, x2, occ, occ, layers, sub)
+    assert list(lists[0]) == [2 * 9 + 2]
+    for l in (1, 2, 3):
+        assert list(lists[l]) == block, l
+    # the value semantics agree
+    w = np.ones((1, 1, 3, 3))
+    ya, yb = SP.forward(x, occ, [w] * 3, layers, sub), SP.forward(x2, occ, [w] * 3, layers, sub)
+    for l, v in enumerate(_value_changed_lists(ya, yb, x, x2)):
+        np.testing.assert_array_equal(v, lists[l])
+    # the misreading does not
+    bad = _lists_of(x, x2, occ, occ, layers, sub, _unmasked_variant)
+    assert sorted(set(bad[3]) - set(block)) == [r * 9 + 5 for r in (1, 2, 3)]
+
+
+_STACKS = [
+    ([(3, 3, 1, False), (3, 3, 1, False), (3, 3, 1, False), (3, 4, 2, False), (4, 4, 1, False)],
+     [False, True, True, False, True]),
+    ([(2, 3, 2, False), (3, 3, 1, False), (3, 3, 1, False), (3, 2, 1, False)],
+     [False, True, True, True]),
+    ([(3, 3, 1, False), (3, 3, 1, False), (3, 3, 2, False), (3, 3, 1, False), (3, 3, 1, False)],
+     [False, False, False, True, True]),
+]
+
+
+@pytest.mark.parametrize("case", range(len(_STACKS)))
+def test_change_sets_equal_value_changes_without_relu(case):
+    """The sparse analogue of the locality pin: with the identity activation,
+    generic weights and generic (never zero) features, a site's value changes
+    exactly when the change rule marks it, at every layer and stride, through
+    refreshes and pillars that appear and vanish.  (ReLU or an all-zero
+    pillar can only make the value set smaller.)  Small sparse grids put
+    submanifold sites next to sites that are empty in both windows, where a
+    wrong restriction of the rule shows."""
+    layers, sub = _STACKS[case]
+    rng = np.random.default_rng(100 + case)
+    H, W, C = 13, 11, layers[0][0]
+    ws = [rng.standard_normal((co, ci, 3, 3)) for (ci, co, _s, _r) in layers]
+    occ = rng.random((H, W)) < 0.12
+    x = np.where(occ[..., None], rng.uniform(0.5, 1.5, (H, W, C)) * rng.choice([-1.0, 1.0], (H, W, C)), 0.0)
+    x = x.astype(np.float32).astype(np.float64)
+    y = SP.forward(x, occ, ws, layers, sub)
+    variant_differs = False
+    for t in range(12):
+        occ2 = occ ^ (rng.random((H, W)) < 0.03)
+        x2 = np.where(occ2[..., None], x, 0.0)
+        fresh = occ2 & ((rng.random((H, W)) < 0.08) | ~occ)
+        x2[fresh] = rng.uniform(0.5, 1.5, (int(fresh.sum()), C)) * rng.choice([-1.0, 1.0], (int(fresh.sum()), C))
+        x2 = x2.astype(np.float32).astype(np.float64)
+        y2 = SP.forward(x2, occ2, ws, layers, sub)
+        lists = _lists_of(x, x2, occ, occ2, layers, sub)
+        vals = _value_changed_lists(y, y2, x, x2)
+        for l in range(len(layers) + 1):
+            np.testing.assert_array_equal(lists[l], vals[l], err_msg=f"stack {case} stride {t} layer {l}")
+        bad = _lists_of(x, x2, occ, occ2, layers, sub, _unmasked_variant)
+        variant_differs |= any(not np.array_equal(b, v) for b, v in zip(bad, vals))
+        x, occ, y = x2, occ2, y2
+    if case == 0:
+        assert variant_differs, "the seeded strides must include a case the unrestricted rule gets wrong"
