@@ -85,17 +85,53 @@ def layer_kernel_name(cin: int, cout: int, stride: int, dtype: str) -> str:
     return f"layer_kernel{'_wide' if wide else ''}<{cin},{cout},{stride},{dtype}>"
 
 
+CONTRACT_SHAPES = {(128, 128), (128, 256), (256, 128), (256, 256)}
+
+
+def layer_split(l: int, wl) -> bool:
+    """Whether layer l (1-based) runs in two launches, the contraction of its
+    changed input rows with all nine taps and the tap sum: the wide stride-1
+    layers after the first."""
+    sp = wl.layers[l - 1]
+    return (l >= 2 and sp.stride == 1 and (sp.cin, sp.cout) in CONTRACT_SHAPES
+            and not int(os.environ.get("SSCATER_FUSED_WIDE", "0") or 0))
+
+
 def kernel_name(slot: int, wl, ups=(), points=False) -> str:
+    """Slots: 0/1 detection, 1 + l layer l (its tap sum when split), then the
+    upsamplers, then L + 1 + n_ups + l the contraction launch of layer l."""
+    L, nu = len(wl.layers), len(ups)
     if slot == 0:
         return "pillar_update_kernel" if points else "detect_kernel<present>"
     if slot == 1:
         return f"pfn_kernel<{wl.dtype}>" if points else "detect_kernel<vanished>"
-    if slot >= len(wl.layers) + 2:
-        u = ups[slot - len(wl.layers) - 2]
+    if slot >= L + 2 + nu:
+        sp = wl.layers[slot - (L + 1 + nu) - 1]
+        return f"contract_kernel<{sp.cin},{sp.cout},{wl.dtype}>"
+    if slot >= L + 2:
+        u = ups[slot - L - 2]
         cin = wl.layers[u.src - 1].cout
         return f"upsample_kernel<{cin},{u.cout},{u.stride},{wl.dtype}>"
-    l = wl.layers[slot - 2]
-    return layer_kernel_name(l.cin, l.cout, l.stride, wl.dtype)
+    l = slot - 1
+    sp = wl.layers[l - 1]
+    if layer_split(l, wl):
+        return f"tap_sum_kernel<{sp.cout},{wl.dtype}>"
+    return layer_kernel_name(sp.cin, sp.cout, sp.stride, wl.dtype)
+
+
+def layer_work(wl, l: int, act, pairs, launches: int):
+    """Algorithmic work of layer l (1-based) over a run: flops, the bytes of
+    the contraction's operands (input delta rows, weights once per launch,
+    input list) and the bytes of the update (Z read + write, emitted deltas,
+    output list and stamps)."""
+    sp = wl.layers[l - 1]
+    L = len(wl.layers)
+    e_d = 4.0                                   # fp32 delta, or the bf16 pair
+    e_w = 2.0 if wl.dtype == "bf16" else 4.0
+    flops = 2.0 * sp.cin * sp.cout * pairs[l]
+    b_c = act[l - 1] * sp.cin * e_d + launches * 9.0 * sp.cin * sp.cout * e_w + 8.0 * act[l - 1]
+    b_s = act[l] * sp.cout * 8.0 + (act[l] * sp.cout * e_d if l < L else 0.0) + 8.0 * act[l]
+    return flops, b_c, b_s
 
 
 def block_times(wl, ms, K: int, n_ups: int = 0) -> dict:
@@ -212,13 +248,15 @@ def cpu_baseline_points(wl, ws, spec, pw, batches, first, budget_s):
 # HBM traffic of the dominant kernel from --pmc FETCH_SIZE / WRITE_SIZE runs
 # scaled by what the same counters read for a plain copy of known size.
 # --------------------------------------------------------------------------
-KERNEL_SOURCES = ("detect.hip", "layer.hip", "misc.hip", "upsample.hip", "pfn.hip", "device_common.h",
-                  "sscater_internal.h")
+KERNEL_SOURCES = ("detect.hip", "layer.hip", "contract.hip", "misc.hip", "upsample.hip", "pfn.hip",
+                  "device_common.h", "sscater_internal.h")
 
 
 # the device-code sources each kernel family is built from
 KERNEL_FILES = {
     "layer_kernel": ("layer.hip", "device_common.h", "sscater_internal.h"),
+    "contract_kernel": ("contract.hip", "device_common.h", "sscater_internal.h"),
+    "tap_sum_kernel": ("contract.hip", "device_common.h", "sscater_internal.h"),
     "detect_kernel": ("detect.hip", "device_common.h", "sscater_internal.h"),
     "upsample_kernel": ("upsample.hip", "device_common.h", "sscater_internal.h"),
     "pfn_kernel": ("pfn.hip", "device_common.h", "sscater_internal.h"),
@@ -296,6 +334,10 @@ def short_kernel(name: str) -> str:
         return f"detect_kernel<{t[0]},{dt(t[1])},{'vanished' if t[2] == 'true' else 'present'}>"
     if fn in ("layer_kernel", "layer_kernel_wide") and len(t) in (4, 5):
         return f"{fn}<{t[0]},{t[1]},{t[2]},{dt(t[3])}>"
+    if fn == "contract_kernel" and len(t) == 3:
+        return f"contract_kernel<{t[0]},{t[1]},{dt(t[2])}>"
+    if fn == "tap_sum_kernel" and len(t) == 3:
+        return f"tap_sum_kernel<{t[0]},{dt(t[1])}>"
     if fn == "pfn_kernel" and len(t) == 1:
         return f"pfn_kernel<{dt(t[0])}>"
     return fn + "<" + ",".join(t) + ">"
@@ -304,7 +346,10 @@ def short_kernel(name: str) -> str:
 def launches_per_stride(kernel: str, wl) -> int:
     if kernel.startswith(("detect_kernel", "pillar_update_kernel", "pfn_kernel")):
         return 1
-    return sum(1 for l in wl.layers if layer_kernel_name(l.cin, l.cout, l.stride, wl.dtype) == kernel)
+    L = len(wl.layers)
+    names = [kernel_name(1 + l, wl) for l in range(1, L + 1)]
+    names += [kernel_name(L + 1 + l, wl) for l in range(1, L + 1) if layer_split(l, wl)]
+    return sum(1 for n in names if n == kernel)
 
 
 def _csv_rows(path):
@@ -877,22 +922,26 @@ def main() -> int:
         a2 = eng.stats()
         pairs2 = [a2["pairs_total"][l] - b2["pairs_total"][l] for l in range(L + 1)]
         act2 = [a2["active_total"][l] - b2["active_total"][l] for l in range(L + 1)]
-        e_d = 4.0
-        for slot in range(L + 2 + len(neck)):
+        nu = len(neck)
+        for slot in range(2 * L + 2 + nu):
             if cnt[slot] == 0:
                 continue
             name = kernel_name(slot, wl, neck, points=spec is not None)
             k = kernels.setdefault(name, {"ms": 0.0, "launches": 0, "flops": 0.0, "bytes": 0.0})
             k["ms"] += ms[slot]
             k["launches"] += cnt[slot]
-            if 2 <= slot < L + 2:
-                l = slot - 1
-                sp = wl.layers[l - 1]
-                k["flops"] += 2.0 * sp.cin * sp.cout * pairs2[l]
-                k["bytes"] += (act2[l - 1] * sp.cin * e_d + act2[l] * sp.cout * 8.0 +
-                               (act2[l] * sp.cout * e_d if l < L else 0.0) +
-                               cnt[slot] * 9.0 * sp.cin * sp.cout * (2 if wl.dtype == "bf16" else 4) +
-                               8.0 * (act2[l - 1] + act2[l]))
+            if 2 <= slot < L + 2 or slot >= L + 2 + nu:
+                contraction = slot >= L + 2 + nu
+                l = slot - (L + 1 + nu) if contraction else slot - 1
+                f, b_c, b_s = layer_work(wl, l, act2, pairs2, cnt[slot])
+                if not layer_split(l, wl):
+                    k["flops"] += f
+                    k["bytes"] += b_c + b_s
+                elif contraction:     # the product carries the flops, its operands the bytes
+                    k["flops"] += f
+                    k["bytes"] += b_c
+                else:                 # the tap sum: Z, emitted deltas, lists
+                    k["bytes"] += b_s
         for name, k in kernels.items():
             log(f"[bench] {name:34s} {k['launches']:5d} launches  avg {k['ms'] / k['launches'] * 1e3:8.2f} us  "
                 f"total {k['ms']:.3f} ms")
@@ -900,7 +949,7 @@ def main() -> int:
         log("[bench] per stride (sum of kernel durations): " +
             ", ".join(f"{k} {v:.1f} us" for k, v in blocks.items()))
         dom_name, dom = max(kernels.items(), key=lambda kv: kv[1]["ms"])
-        if dom["flops"] > 0:
+        if dom["flops"] > 0 or dom["bytes"] > 0:
             # start and end stamped by the kernel's own dispatch packet
             launch_us = dom["ms"] / dom["launches"] * 1e3
             secs = launch_us * 1e-6 * dom["launches"]

@@ -293,13 +293,16 @@ int sscater_stats(sscater_t h, sscater_stats_t* out, void* stream);
  * the figure is the kernel's execution time without the event packets' cost.
  * Slots: 0 = input change detection (present pillars; points mode: the pillar
  * queue update), 1 = vanished pillars (points mode: the feature net),
- * 1 + l = layer l (l = 1..L), L + 2 + u = upsampler u of the neck, so
- * L + 2 + n_ups slots in all.  Enable it only for runs that measure kernels. */
+ * 1 + l = layer l (l = 1..L; for a wide stride-1 layer that runs in two
+ * launches, its tap sum), L + 2 + u = upsampler u of the neck, and
+ * L + 1 + n_ups + l = the contraction launch of layer l when it has one, so
+ * 2L + 2 + n_ups slots in all.  Enable it only for runs that measure
+ * kernels. */
 int sscater_profile(sscater_t h, int32_t enable);
 
 /* Sum of the timed launch durations per slot (milliseconds) and the number of
  * launches per slot since the previous read, into host arrays of
- * n >= L + 2 + n_ups entries; clears the record.  Synchronises `stream`. */
+ * n >= 2L + 2 + n_ups entries; clears the record.  Synchronises `stream`. */
 int sscater_profile_read(sscater_t h, double* ms, int64_t* launches, int32_t n, void* stream);
 
 /* Static text for an error code; for SSCATER_E_HIP the last HIP error text of

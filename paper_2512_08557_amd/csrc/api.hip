@@ -50,6 +50,10 @@ struct LayerState {
     // layer, shared with the submanifold layers of its block)
     uint64_t* memb = nullptr;
     bool sub = false;
+    // wide stride-1 layers after the first: two launches, the contraction of
+    // the changed input rows with all nine taps, then the tap sum
+    bool split = false;
+    void* wg = nullptr;      // contraction weights [9*cout][cin]
 };
 
 // One upsampler of the neck.
@@ -88,6 +92,8 @@ struct sscater {
     int Hn = 0, Wn = 0, Cn = 0;
     float* Zn = nullptr;
     uint32_t* stamp_n = nullptr;
+    float* part = nullptr;         // tap contributions of a split layer, dense by cell (shared by those layers)
+    float* zero = nullptr;         // a zero row of 9 * max cout floats
     void* X = nullptr;
     uint64_t* pres = nullptr;
     uint32_t* stamp0 = nullptr;
@@ -264,9 +270,29 @@ int run_layers(sscater* h, int set, uint32_t epoch, hipStream_t s) {
             a.cum_dst = h->cum;
             a.n_cum = h->ncnt();
         }
-        e = timed_launch(h, 1 + l, s, [&](const LaunchCtx& c) {
-            return launch_layer(a, ls.spec.cin, ls.spec.cout, ls.spec.stride, h->bf16, h->sparse, h->layer_grid, c);
-        });
+        if (ls.split) {
+            ContractArgs g{};
+            g.list = h->layers[l - 2].list;
+            g.count = h->cnt_ptr(set, l - 1);
+            g.cap = (int)h->cells_of(l - 1);
+            g.delta_in = a.delta_in;
+            g.wg = ls.wg;
+            g.part = h->part;
+            e = timed_launch(h, h->L + 1 + h->n_ups + l, s, [&](const LaunchCtx& c) {
+                return launch_contract(g, ls.spec.cin, ls.spec.cout, h->bf16, h->layer_grid, c);
+            });
+            if (e != hipSuccess) return hip_fail(e);
+            a.part = h->part;
+            a.zero = h->zero;
+            e = timed_launch(h, 1 + l, s, [&](const LaunchCtx& c) {
+                return launch_tap_sum(a, ls.spec.cout, h->bf16, h->sparse, h->layer_grid, c);
+            });
+        } else {
+            e = timed_launch(h, 1 + l, s, [&](const LaunchCtx& c) {
+                return launch_layer(a, ls.spec.cin, ls.spec.cout, ls.spec.stride, h->bf16, h->sparse, h->layer_grid,
+                                    c);
+            });
+        }
         if (e != hipSuccess) return hip_fail(e);
     }
 
@@ -397,6 +423,10 @@ int create_impl(const sscater_grid* grid, int32_t batch, const sscater_layer* la
 
     int rc = SSCATER_OK;
     const size_t esz = bf16 ? 2 : 4;
+    // SSCATER_FUSED_WIDE=1 keeps every wide stride-1 layer in the one-launch
+    // output-stationary kernel (for comparing the two forms)
+    const char* fw = getenv("SSCATER_FUSED_WIDE");
+    const bool split_wide = !(fw && atoi(fw) != 0);
     const size_t cells = (size_t)cells0;
 #define SSC_TRY(expr)                 \
     do {                              \
@@ -414,6 +444,7 @@ int create_impl(const sscater_grid* grid, int32_t batch, const sscater_layer* la
     SSC_TRY(dev_alloc(h, (void**)&h->cum, (size_t)h->ncnt() * 8));
     {
         int H = grid->H, W = grid->W;
+        size_t part_bytes = 0, zero_bytes = 0;
         for (int l = 0; l < n_layers; ++l) {
             LayerState& ls = h->layers[l];
             ls.spec = layers[l];
@@ -428,14 +459,32 @@ int create_impl(const sscater_grid* grid, int32_t batch, const sscater_layer* la
             bool feeds_up = false;
             for (int u = 0; u < n_ups; ++u) feeds_up = feeds_up || ups[u].src_layer == l + 1;
             if (l + 1 < n_layers || feeds_up) SSC_TRY(dev_alloc(h, &ls.delta, oc * ls.spec.cout * 4));
-            const size_t wn = wpack_elems(ls.spec.cin, ls.spec.cout, bf16);
-            std::vector<unsigned char> packed(wn * esz);
-            pack_weights(weights[l], ls.spec.cin, ls.spec.cout, bf16, packed.data());
-            SSC_TRY(dev_alloc(h, &ls.wpack, wn * esz));
-            he = hipMemcpy(ls.wpack, packed.data(), wn * esz, hipMemcpyHostToDevice);
-            if (he != hipSuccess) { rc = hip_fail(he); goto fail; }
+            // the first layer's input list is not built (detection propagates
+            // A_0 straight into A_1), so it always takes the one-launch kernel
+            ls.split = l > 0 && split_wide && contract_supported(ls.spec.cin, ls.spec.cout, ls.spec.stride, bf16);
+            if (ls.split) {
+                const size_t wn = (size_t)9 * ls.spec.cout * ls.spec.cin;
+                std::vector<unsigned char> packed(wn * esz);
+                pack_contract_weights(weights[l], ls.spec.cin, ls.spec.cout, bf16, packed.data());
+                SSC_TRY(dev_alloc(h, &ls.wg, wn * esz));
+                he = hipMemcpy(ls.wg, packed.data(), wn * esz, hipMemcpyHostToDevice);
+                if (he != hipSuccess) { rc = hip_fail(he); goto fail; }
+                part_bytes = std::max(part_bytes, (size_t)batch * H * W * 9 * ls.spec.cout * 4);
+                zero_bytes = std::max(zero_bytes, (size_t)9 * ls.spec.cout * 4);
+            } else {
+                const size_t wn = wpack_elems(ls.spec.cin, ls.spec.cout, bf16);
+                std::vector<unsigned char> packed(wn * esz);
+                pack_weights(weights[l], ls.spec.cin, ls.spec.cout, bf16, packed.data());
+                SSC_TRY(dev_alloc(h, &ls.wpack, wn * esz));
+                he = hipMemcpy(ls.wpack, packed.data(), wn * esz, hipMemcpyHostToDevice);
+                if (he != hipSuccess) { rc = hip_fail(he); goto fail; }
+            }
             H = ls.Hout;
             W = ls.Wout;
+        }
+        if (part_bytes) {
+            SSC_TRY(dev_alloc(h, (void**)&h->part, part_bytes));
+            SSC_TRY(dev_alloc(h, (void**)&h->zero, zero_bytes));
         }
     }
     if (n_ups > 0) {
@@ -958,7 +1007,7 @@ int sscater_profile(sscater_t h, int32_t enable) {
 }
 
 int sscater_profile_read(sscater_t h, double* ms, int64_t* launches, int32_t n, void* stream) {
-    if (!h || !ms || !launches || n < h->L + 2 + h->n_ups) return SSCATER_E_INVALID_ARG;
+    if (!h || !ms || !launches || n < 2 * h->L + 2 + h->n_ups) return SSCATER_E_INVALID_ARG;
     DeviceGuard dg(h->device);
     if (!dg.ok) return hip_fail(hipGetLastError());
     hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));

@@ -204,6 +204,47 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
     return u >> 16;
 }
 
+// Z update and next-layer delta row of one lane: output cell q, output
+// channels co0 .. co0+3 (fp32 Z_new = Z_old + D; delta phi(Z_new) -
+// phi(Z_old), or the bf16 pair [bf16(phi(Z_new)) | bf16(phi(Z_old))]).
+// Sparse backbones: now / prev say whether the site is active in this and
+// in the previous stride; an inactive site's output is zero.
+template <int COUT, bool BF16>
+__device__ __forceinline__ void epilogue4(const LayerArgs& a, int q, int co0, const f4v o, const f4v d,
+                                          bool now = true, bool prev = true) {
+    f4v zn;
+    zn.x = o.x + d.x;
+    zn.y = o.y + d.y;
+    zn.z = o.z + d.z;
+    zn.w = o.w + d.w;
+    *reinterpret_cast<f4v*>(a.Z + (size_t)q * COUT + co0) = zn;
+    if (!a.delta_out) return;
+    f4v yo = o, yn = zn;
+    if (a.relu) {
+        yo.x = fmaxf(yo.x, 0.f); yo.y = fmaxf(yo.y, 0.f); yo.z = fmaxf(yo.z, 0.f); yo.w = fmaxf(yo.w, 0.f);
+        yn.x = fmaxf(yn.x, 0.f); yn.y = fmaxf(yn.y, 0.f); yn.z = fmaxf(yn.z, 0.f); yn.w = fmaxf(yn.w, 0.f);
+    }
+    if (!prev) yo = f4v{0.f, 0.f, 0.f, 0.f};
+    if (!now) yn = f4v{0.f, 0.f, 0.f, 0.f};
+    char* drow = static_cast<char*>(a.delta_out) + (size_t)q * (4 * COUT);
+    if constexpr (BF16) {
+        uint2 pn, po;
+        pn.x = f32_to_bf16_bits(yn.x) | (f32_to_bf16_bits(yn.y) << 16);
+        pn.y = f32_to_bf16_bits(yn.z) | (f32_to_bf16_bits(yn.w) << 16);
+        po.x = f32_to_bf16_bits(yo.x) | (f32_to_bf16_bits(yo.y) << 16);
+        po.y = f32_to_bf16_bits(yo.z) | (f32_to_bf16_bits(yo.w) << 16);
+        *reinterpret_cast<uint2*>(drow + co0 * 2) = pn;
+        *reinterpret_cast<uint2*>(drow + COUT * 2 + co0 * 2) = po;
+    } else {
+        f4v dy;
+        dy.x = yn.x - yo.x;
+        dy.y = yn.y - yo.y;
+        dy.z = yn.z - yo.z;
+        dy.w = yn.w - yo.w;
+        *reinterpret_cast<f4v*>(drow + co0 * 4) = dy;
+    }
+}
+
 __device__ __forceinline__ void flag_error(int32_t* err, int bit) {
     *(volatile int32_t*)err = bit;
 }

@@ -101,6 +101,23 @@ struct LayerArgs {
     const int32_t* cum_src;     // this stride's counters [n_cum]
     long long* cum_dst;         // totals [n_cum]
     int n_cum;
+    // layers contracted in two launches (tap_sum_kernel): the tap
+    // contributions of the changed input cells, dense by cell
+    // [Hin*Win][9][cout] fp32, and a zero row of 9*cout floats that stands
+    // in for an unchanged input
+    const float* part;
+    const float* zero;
+};
+
+// The scatter form of Eq. 2 for one stride-1 layer: every changed input row
+// times the weights of all nine taps, [|A_{l-1}| x cin] x [cin x 9*cout].
+struct ContractArgs {
+    const int32_t* list;        // A_{l-1}: NSHARD segments of `cap` cells of the input grid
+    const int32_t* count;       // segment lengths, segment k at count[k * CSTRIDE]
+    int cap;
+    const void* delta_in;       // input deltas, dense by cell [Hin*Win][4*cin bytes]
+    const void* wg;             // weights [9*cout][cin] (fp32, or bf16 values), row tap*cout + co
+    float* part;                // tap contributions, dense by cell [Hin*Win][9*cout]
 };
 
 // One upsampler of the neck: transposed convolution (kernel = stride) of a
@@ -201,6 +218,14 @@ hipError_t launch_read_masked(const float* Z, void* dst, long long cells, int co
 // channels of a [cells][ctot] destination.
 hipError_t launch_read_slice(const float* Z, void* dst, long long cells, int ctot, int coff, int cout, int relu,
                              bool bf16, hipStream_t s);
+// Wide stride-1 layers: the contraction of the changed input rows with all
+// nine taps into `part`, then the output-stationary sum of the tap
+// contributions with the Z update, the delta epilogue and the propagation.
+bool contract_supported(int cin, int cout, int stride, bool bf16);
+hipError_t launch_contract(const ContractArgs& a, int cin, int cout, bool bf16, int grid, const LaunchCtx& c);
+hipError_t launch_tap_sum(const LayerArgs& a, int cout, bool bf16, bool sparse, int grid, const LaunchCtx& c);
+// [9*cout][cin] contraction weights from OIHW (fp32 values, or bf16 bits).
+void pack_contract_weights(const void* w_oihw, int cin, int cout, bool bf16, void* dst);
 bool upsample_supported(int cin, int cout, int stride);
 hipError_t launch_upsample(const UpArgs& a, int cin, int cout, int stride, bool bf16, int grid,
                            const LaunchCtx& c);

@@ -297,9 +297,10 @@ class Engine:
         _check(lib().sscater_profile(self._h, int(bool(enable))), "sscater_profile")
 
     def profile_read(self, stream=None):
-        """(ms per slot, launches per slot); slot 0 detect, 1 vanished, 1+l layer l,
-        L+2+u upsampler u."""
-        n = len(self.layers) + 2 + len(self.ups)
+        """(ms per slot, launches per slot); slot 0 detect, 1 vanished, 1+l layer l
+        (for a layer contracted in two launches: its tap sum), L+2+u upsampler u,
+        L+1+n_ups+l the contraction launch of layer l when it has one."""
+        n = 2 * len(self.layers) + 2 + len(self.ups)
         ms = (ctypes.c_double * n)()
         cnt = (ctypes.c_int64 * n)()
         _check(lib().sscater_profile_read(self._h, ms, cnt, n, self._stream(stream)), "sscater_profile_read")
