@@ -67,7 +67,8 @@ enum {
     SSCATER_E_OUT_OF_MEMORY = -2, /* device or host allocation failed */
     SSCATER_E_HIP = -3,           /* HIP runtime error (text via sscater_strerror) */
     SSCATER_E_OVERFLOW = -4,      /* more pillars than max_pillars: no sampling, the stride is refused */
-    SSCATER_E_DEVICE = -5         /* sticky device-side input fault (see above) */
+    SSCATER_E_DEVICE = -5,        /* sticky device-side input fault (see above) */
+    SSCATER_E_SCRATCH = -6        /* the grid is larger than the fixed scratch of an allocation-free call */
 };
 
 typedef enum { SSCATER_F32 = 0, SSCATER_BF16 = 1 } sscater_dtype;
@@ -277,6 +278,24 @@ int sscater_destroy(sscater_t h);
  * dst with cap > 0; SSCATER_E_DEVICE when the sticky flag is set. */
 int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32_t* count_host,
                     void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * list as sscater_changed (the last stride's A_layer, sorted row-major), built
+ * on the device into the caller's DEVICE buffer dst[cap], with its length
+ * written to the DEVICE int *count (also when it exceeds cap, in which case
+ * only cap entries are written).  Asynchronous on `stream`: the call enqueues
+ * three kernels and returns; nothing is synchronised, allocated or freed, so
+ * the call can be captured into a graph.  The kernels keep per-block counts
+ * in a fixed device array of the library (256 KB per GPU, held until the
+ * process ends), which limits the layer's grid to 64 Mi cells (whole batch);
+ * a larger grid is refused with SSCATER_E_SCRATCH before anything is
+ * enqueued.  Calls that overlap on one GPU (concurrent streams or threads)
+ * share that array and race: order them on one stream.  Errors:
+ * SSCATER_E_INVALID_ARG for a null handle or count, a layer out of range,
+ * cap < 0 or a null dst with cap > 0; SSCATER_E_DEVICE when the sticky flag
+ * is set; SSCATER_E_HIP for a launch failure. */
+int sscater_changed_noalloc(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32_t* count, void* stream);
 
 /* Test / metrics extension: counters of the last stride and totals into the
  * host struct *out: |A_l| per layer (the sizes of Alg. 1's change maps), the

@@ -331,6 +331,7 @@ const char* sscater_strerror(int code) {
         case SSCATER_E_OUT_OF_MEMORY: return "out of memory";
         case SSCATER_E_HIP: return g_hip_err;
         case SSCATER_E_OVERFLOW: return "pillar count exceeds max_pillars (no sampling)";
+        case SSCATER_E_SCRATCH: return "grid larger than the fixed scratch of an allocation-free call (64 Mi cells)";
         case SSCATER_E_DEVICE:
             return "device-side input fault (cell index out of range, duplicate cell, or a pillar over its point "
                    "capacity)";
@@ -865,6 +866,38 @@ int sscater_destroy(sscater_t h) {
     delete h;
     return SSCATER_OK;
 }
+
+}  // extern "C"
+
+namespace ssc {
+
+int report_hip_error(hipError_t e) { return hip_fail(e); }
+
+int changed_source(const sscater* h, int layer, ChangedSource* out) {
+    if (!h || !out || layer < 0 || layer > h->L + (h->n_ups > 0 ? 1 : 0)) return SSCATER_E_INVALID_ARG;
+    if (int rc = check_sticky(h)) return rc;
+    ChangedSource c;
+    c.device = h->device;
+    c.have = h->last_set >= 0;
+    c.epoch = h->last_epoch;
+    if (layer == 0) {
+        c.stamp = h->stamp0;
+        c.cells = (long long)h->cells_of(0);
+    } else if (layer == h->L + 1) {
+        c.stamp = h->stamp_n;
+        c.cells = (long long)h->Hn * h->Wn;
+    } else {
+        c.stamp = h->layers[layer - 1].stamp;
+        c.cells = (long long)h->cells_of(layer);
+        if (h->sparse) c.memb = h->layers[layer - 1].memb;
+    }
+    *out = c;
+    return SSCATER_OK;
+}
+
+}  // namespace ssc
+
+extern "C" {
 
 int sscater_changed(sscater_t h, int32_t layer, int32_t* dst, int32_t cap, int32_t* count_host, void* stream) {
     if (!h || !count_host || layer < 0 || layer > h->L + (h->n_ups > 0 ? 1 : 0) || cap < 0 || (cap > 0 && !dst))

@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+struct sscater;   // the handle (api.hip)
+
 namespace ssc {
 
 // Change sets.  A cell q of a grid belongs to the current stride's set when
@@ -188,6 +190,23 @@ struct PfnArgs {
 };
 
 enum ErrBits { ERR_INDEX_RANGE = 1, ERR_DUPLICATE = 2, ERR_PILLAR_FULL = 4 };
+
+// What a layer's change list is made of, for the device-side list: the cells
+// q of the layer's grid with stamp[q] == epoch, restricted for a sparse layer
+// to the sites active now or in the previous stride.
+struct ChangedSource {
+    const uint32_t* stamp = nullptr;
+    const uint64_t* memb = nullptr;   // sparse layers only
+    uint32_t epoch = 0;
+    long long cells = 0;              // cells of the grid (whole batch)
+    int device = 0;
+    bool have = false;                // a stride has run since create / reset
+};
+// SSCATER_OK, SSCATER_E_INVALID_ARG (null handle, layer out of range) or
+// SSCATER_E_DEVICE (sticky device fault).
+int changed_source(const sscater* h, int layer, ChangedSource* out);
+// Record a HIP error for sscater_strerror; returns the matching error code.
+int report_hip_error(hipError_t e);
 
 // Where a launch goes: its stream and, while kernel timing is on, two events
 // that the dispatch packet itself stamps when the kernel starts and ends

@@ -19,15 +19,15 @@ LIB_PATH = os.path.join(_HERE, "libsscater.so")
 
 MAX_LAYERS = 32
 MAX_UPSAMPLERS = 4
-OK, E_INVALID_ARG, E_OUT_OF_MEMORY, E_HIP, E_OVERFLOW, E_DEVICE = 0, -1, -2, -3, -4, -5
+OK, E_INVALID_ARG, E_OUT_OF_MEMORY, E_HIP, E_OVERFLOW, E_DEVICE, E_SCRATCH = 0, -1, -2, -3, -4, -5, -6
 F32, BF16 = 0, 1
 
 # every function declared in include/sscater.h
 EXPORTS = ("sscater_create", "sscater_create_neck", "sscater_create_pfn", "sscater_create_sparse",
            "sscater_create_batched", "sscater_step",
            "sscater_step_points",
-           "sscater_read", "sscater_reset", "sscater_destroy", "sscater_changed", "sscater_stats", "sscater_profile",
-           "sscater_profile_read", "sscater_strerror")
+           "sscater_read", "sscater_reset", "sscater_destroy", "sscater_changed", "sscater_changed_noalloc",
+           "sscater_stats", "sscater_profile", "sscater_profile_read", "sscater_strerror")
 
 
 class Grid(ctypes.Structure):
@@ -97,6 +97,7 @@ def lib() -> ctypes.CDLL:
         L.sscater_reset.argtypes = [vp, vp]
         L.sscater_destroy.argtypes = [vp]
         L.sscater_changed.argtypes = [vp, i32, ctypes.POINTER(i32), i32, ctypes.POINTER(i32), vp]
+        L.sscater_changed_noalloc.argtypes = [vp, i32, vp, i32, vp, vp]
         L.sscater_stats.argtypes = [vp, ctypes.POINTER(Stats), vp]
         L.sscater_profile.argtypes = [vp, i32]
         L.sscater_profile_read.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64), i32,
@@ -283,6 +284,20 @@ class Engine:
         _check(lib().sscater_changed(self._h, layer, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), cap,
                                      ctypes.byref(cnt), self._stream(stream)), "sscater_changed")
         return buf[:cnt.value].copy()
+
+    def changed_noalloc(self, layer: int, dst, count, stream=None) -> None:
+        """The last stride's sorted change list of `layer` into the int32 cuda
+        tensor dst (its capacity is dst.numel()) and its length into the
+        one-element int32 cuda tensor count, enqueued on the stream; the
+        library allocates nothing."""
+        for t in (dst, count):
+            if t.dtype != self._torch.int32 or not t.is_cuda or not t.is_contiguous():
+                raise ValueError("dst and count must be contiguous int32 cuda tensors")
+        if count.numel() < 1:
+            raise ValueError("count needs one element")
+        _check(lib().sscater_changed_noalloc(self._h, layer, ctypes.c_void_p(dst.data_ptr()), dst.numel(),
+                                             ctypes.c_void_p(count.data_ptr()), self._stream(stream, (dst, count))),
+               "sscater_changed_noalloc")
 
     def stats(self, stream=None) -> Dict:
         st = Stats()

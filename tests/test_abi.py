@@ -243,3 +243,10 @@ def test_create_batched_rejects_invalid_batch(batch, hw):
     wp = (ctypes.c_void_p * 1)(buf.ctypes.data)
     h = ctypes.c_void_p()
     assert lib.sscater_create_batched(ctypes.byref(g), batch, larr, 1, wp, ctypes.byref(h)) == ssc.E_INVALID_ARG
+
+
+def test_noalloc_change_list_rejects_bad_arguments_on_the_host():
+    lib = ssc.lib()
+    cnt = ctypes.c_void_p(8)   # never dereferenced: every case fails validation first
+    assert lib.sscater_changed_noalloc(None, 0, None, 0, cnt, None) == ssc.E_INVALID_ARG
+    assert b"scratch" in lib.sscater_strerror(E.E_SCRATCH)
