@@ -51,16 +51,27 @@ struct CShape {
     static constexpr int ESZ = BF16 ? 2 : 4;         // bytes of a stored element
     static constexpr int N = 9 * COUT;               // product columns: (tap, output channel)
     static constexpr int NT = N / 64;                // 64-column tiles
+    // rows per tile: 64 (four wavefronts of 32 x 32).  Measured against
+    // 32-row tiles (two wavefronts, six workgroups per compute unit): the
+    // same launch time, at twice the weight traffic from L2
+    static constexpr int MT = 64;
+    static constexpr int NW = 2 * MT / 32;           // wavefronts: MT/32 x 2 quadrants of 32 x 32
     static constexpr int NCH = CIN * ESZ / 128;      // 128-byte chunks of a cin row
     static constexpr int NA = BF16 ? 2 : 1;          // A operands: the fp32 delta, or the new and old halves
     static constexpr int ROWB = 4 * CIN;             // bytes of an input delta row
     static constexpr int WROWB = CIN * ESZ;          // bytes of a weight row
-    static constexpr int OPB = 64 * 128;             // one operand of one chunk: 64 rows x 128 bytes
-    static constexpr int STB = (NA + 1) * OPB;       // one stage
-    // stages in the ring: fp32 keeps three chunks in flight behind the one
-    // being contracted (64 KB, two workgroups per compute unit), bf16 one
-    static constexpr int S = BF16 ? (NCH >= 3 ? 3 : NCH) : (NCH >= 4 ? 4 : NCH);
-    static constexpr int LPC = 2 * (NA + 1);         // copies per thread per chunk
+    static constexpr int OPA = MT * 128;             // one A operand of one chunk: MT rows x 128 bytes
+    static constexpr int OPBB = 64 * 128;            // the B operand of one chunk: 64 rows x 128 bytes
+    static constexpr int STB = NA * OPA + OPBB;      // one stage
+    // stages in the ring: 48 KB of LDS, so three workgroups share a compute
+    // unit and the ~400-650 tiles of a 432x496 backbone layer are resident at
+    // once (with 64 KB, two per unit, a second round of tiles started only as
+    // the first ended); fp32 keeps two chunks in flight behind the one being
+    // contracted, bf16 (24 KB per stage) one
+    static constexpr int S = BF16 ? 2 : 3;
+    static constexpr int BPW = 8 / NW;               // B blocks (1 KB) each wavefront copies per chunk
+    static constexpr int LPC = 2 * NA + BPW;         // copies per thread per chunk
+    static constexpr int SLOTS = 768;                // resident workgroups on 256 compute units
     static_assert(N % 64 == 0 && NCH >= 2, "shape");
 };
 
@@ -108,28 +119,27 @@ __device__ __forceinline__ void copy16(const void* src, void* lds) {
 
 // plist, pcount, pcap: preloaded copies of a.list, a.count, a.cap.
 template <int CIN, int COUT, bool BF16>
-__global__ __launch_bounds__(256) void contract_kernel(const int32_t* __restrict__ plist,
-                                                        const int32_t* __restrict__ pcount, int pcap,
-                                                        ContractArgs a) {
+__global__ __launch_bounds__((64 * CShape<CIN, COUT, BF16>::NW)) void contract_kernel(
+    const int32_t* __restrict__ plist, const int32_t* __restrict__ pcount, int pcap, ContractArgs a) {
     using C = CShape<CIN, COUT, BF16>;
+    constexpr int MT = C::MT, NW = C::NW;
     // one LDS array per stage: the compiler then tracks the copies into each
     // stage separately and waits only for those a read depends on
     __shared__ __attribute__((aligned(1024))) char st0[C::STB];
     __shared__ __attribute__((aligned(1024))) char st1[C::S > 1 ? C::STB : 16];
     __shared__ __attribute__((aligned(1024))) char st2[C::S > 2 ? C::STB : 16];
-    __shared__ __attribute__((aligned(1024))) char st3[C::S > 3 ? C::STB : 16];
-    __shared__ int rowcell[64];
+    __shared__ int rowcell[MT];
 
     const int tid = (int)threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = w & 1, wn = w >> 1;                 // this wavefront's 32 x 32 quadrant
+    const int wm = w % (MT / 32), wn = w / (MT / 32);  // this wavefront's 32 x 32 quadrant
     const int li = lane & 31, kg = lane >> 5;
     const int n0 = pcount[0], n1 = pcount[CSTRIDE];
-    const int mt0 = (n0 + 63) >> 6;
-    const int total = (mt0 + ((n1 + 63) >> 6)) * C::NT;
-    // copy roles: wavefront w fills 1 KB blocks w and 4 + w of every operand,
-    // block k holding rows 8k .. 8k+7; lane l takes row 8k + l/8 and the
-    // 16-byte piece (l % 8) ^ (l / 8) of it, landing in slot l % 8
+    const int mt0 = (n0 + MT - 1) / MT;
+    const int total = (mt0 + (n1 + MT - 1) / MT) * C::NT;
+    // copy roles: 1 KB blocks of 8 rows; wavefront w fills A blocks w and
+    // NW + w, and B blocks w + j*NW; lane l takes row 8k + l/8 of block k and
+    // the 16-byte piece (l % 8) ^ (l / 8) of it, landing in slot l % 8
     const int cr = lane >> 3;
     const int piece = (lane & 7) ^ cr;
     const char* dsrc = static_cast<const char*>(a.delta_in) + piece * 16;
@@ -138,33 +148,35 @@ __global__ __launch_bounds__(256) void contract_kernel(const int32_t* __restrict
     for (int t = (int)blockIdx.x; t < total; t += (int)gridDim.x) {
         const int mt = t / C::NT, nt = t - mt * C::NT;
         const int seg = mt < mt0 ? 0 : 1;
-        const int base = (mt - (seg ? mt0 : 0)) * 64;
+        const int base = (mt - (seg ? mt0 : 0)) * MT;
         const int nseg = seg ? n1 : n0;
         const int32_t* lst = plist + (size_t)seg * pcap;
         // rows past the segment's end copy row `base` (always valid) and are
         // never stored: a row of the product depends on its own A row only
-        const int r0 = 8 * w + cr, r1 = r0 + 32;
+        const int r0 = 8 * w + cr, r1 = 8 * (NW + w) + cr;
         const int cell0 = lst[base + (base + r0 < nseg ? r0 : 0)];
         const int cell1 = lst[base + (base + r1 < nseg ? r1 : 0)];
-        if (tid < 64) rowcell[tid] = base + tid < nseg ? lst[base + tid] : -1;
+        if (tid < MT) rowcell[tid] = base + tid < nseg ? lst[base + tid] : -1;
         const char* a0 = dsrc + (size_t)cell0 * C::ROWB;
         const char* a1 = dsrc + (size_t)cell1 * C::ROWB;
-        const char* b0 = wsrc + (size_t)(nt * 64 + r0) * C::WROWB;
-        const char* b1 = wsrc + (size_t)(nt * 64 + r1) * C::WROWB;
+        const char* bsrc = wsrc + (size_t)(nt * 64 + cr) * C::WROWB;
 
         auto issue = [&](int c, char* stp) __attribute__((always_inline)) {
             char* d0 = stp + w * 1024;
-            char* d1 = stp + (4 + w) * 1024;
+            char* d1 = stp + (NW + w) * 1024;
             copy16(a0 + c * 128, d0);
             copy16(a1 + c * 128, d1);
             if constexpr (BF16) {   // the old half of the pair row
-                copy16(a0 + 2 * CIN + c * 128, d0 + C::OPB);
-                copy16(a1 + 2 * CIN + c * 128, d1 + C::OPB);
+                copy16(a0 + 2 * CIN + c * 128, d0 + C::OPA);
+                copy16(a1 + 2 * CIN + c * 128, d1 + C::OPA);
             }
-            copy16(b0 + c * 128, d0 + C::NA * C::OPB);
-            copy16(b1 + c * 128, d1 + C::NA * C::OPB);
+#pragma unroll
+            for (int j = 0; j < C::BPW; ++j) {
+                const int k = w + j * NW;            // B block: rows 8k .. 8k+7
+                copy16(bsrc + (size_t)(8 * k) * C::WROWB + c * 128, stp + C::NA * C::OPA + k * 1024);
+            }
         };
-        auto stage = [&](int k) -> char* { return k == 0 ? st0 : (k == 1 ? st1 : (k == 2 ? st2 : st3)); };
+        auto stage = [&](int k) -> char* { return k == 0 ? st0 : (k == 1 ? st1 : st2); };
 
         f16v acc = {};
         f16v acc_old = {};
@@ -177,9 +189,9 @@ __global__ __launch_bounds__(256) void contract_kernel(const int32_t* __restrict
             for (int g = 0; g < 4; ++g) {
                 const int c16 = 2 * g + kg;
                 av[g] = *reinterpret_cast<const uint4*>(stp + ra * 128 + 16 * (c16 ^ (ra & 7)));
-                bv[g] = *reinterpret_cast<const uint4*>(stp + C::NA * C::OPB + rb * 128 + 16 * (c16 ^ (rb & 7)));
+                bv[g] = *reinterpret_cast<const uint4*>(stp + C::NA * C::OPA + rb * 128 + 16 * (c16 ^ (rb & 7)));
                 if constexpr (BF16)
-                    ov[g] = *reinterpret_cast<const uint4*>(stp + C::OPB + ra * 128 + 16 * (c16 ^ (ra & 7)));
+                    ov[g] = *reinterpret_cast<const uint4*>(stp + C::OPA + ra * 128 + 16 * (c16 ^ (ra & 7)));
             }
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
@@ -341,14 +353,19 @@ bool contract_supported(int cin, int cout, int stride, bool /*bf16*/) {
     return false;
 }
 
+template <int CI, int CO, bool BF16>
+static hipError_t launch_ct(const ContractArgs& a, int grid, const LaunchCtx& c) {
+    using C = CShape<CI, CO, BF16>;
+    // as many workgroups as are resident at once; a larger list loops over
+    // its remaining tiles
+    (void)grid;
+    grid = C::SLOTS;
+    return launch_kernel(c, contract_kernel<CI, CO, BF16>, dim3(grid), dim3(64 * C::NW), a.list, a.count, a.cap, a);
+}
+
 hipError_t launch_contract(const ContractArgs& a, int cin, int cout, bool bf16, int grid, const LaunchCtx& c) {
-    grid = std::max(8, grid / 8 * 8);
-#define SSC_CL(CI, CO)                                                                                            \
-    if (cin == CI && cout == CO)                                                                                  \
-        return bf16 ? launch_kernel(c, contract_kernel<CI, CO, true>, dim3(grid), dim3(256), a.list, a.count, a.cap, \
-                                    a)                                                                            \
-                    : launch_kernel(c, contract_kernel<CI, CO, false>, dim3(grid), dim3(256), a.list, a.count, a.cap, \
-                                    a);
+#define SSC_CL(CI, CO) \
+    if (cin == CI && cout == CO) return bf16 ? launch_ct<CI, CO, true>(a, grid, c) : launch_ct<CI, CO, false>(a, grid, c);
     SSC_CONTRACT_SHAPES(SSC_CL)
 #undef SSC_CL
     return hipErrorInvalidValue;
