@@ -102,3 +102,61 @@ class DeltaScatterModel:
             lists.append(a_next)
             a_prev, d_prev = a_next, d_next
         return lists
+
+
+class DeltaFormModel:
+    """Vectorised model of the method for the bf16 storage case, used to
+    measure how the form of the delta affects drift against recomputation
+    (the delta-form question of the bf16 case).
+
+    Per stride: the input delta is the exact difference of the two canvases;
+    for each layer the persistent pre-activation map takes Z += conv(delta)
+    (Eq. 2 summed over the taps: the scatter of every changed site, as one
+    dense convolution of a map that is zero off the changed sites), kept in
+    float32 (`z32`, one rounding per stride) or float64; the stored output is
+    bf16(phi(Z)) and the next layer's delta is
+      delta="pair":    bf16(phi(Z_new)) - bf16(phi(Z_old)) exactly (the
+                       difference of two bf16 values, carried as the pair);
+      delta="rounded": that difference rounded to bf16 before the scatter.
+    """
+
+    def __init__(self, layers: Sequence[Tuple[int, int, int, bool]], weights: Sequence[np.ndarray],
+                 delta: str = "pair", z32: bool = True):
+        from . import conv3x3
+        assert delta in ("pair", "rounded")
+        self._conv = conv3x3
+        self.layers = [tuple(l) for l in layers]
+        self.w = [np.asarray(w, dtype=np.float64) for w in weights]
+        self.delta = delta
+        self.z32 = z32
+        self.x = None
+        self.z = None
+
+    def _phi(self, l: int, z: np.ndarray) -> np.ndarray:
+        y = np.maximum(z, 0.0) if self.layers[l][3] else z
+        return round_bf16(y)
+
+    def step(self, x_new: np.ndarray) -> List[np.ndarray]:
+        """Advance one window (x_new: the canvas's exact values); return the
+        stored outputs Y_1..Y_L."""
+        x_new = np.asarray(x_new, dtype=np.float64)
+        if self.x is None:
+            self.x = np.zeros_like(x_new)
+        d = x_new - self.x
+        self.x = x_new.copy()
+        ys = []
+        zs = []
+        for l, (_ci, _co, s, _r) in enumerate(self.layers):
+            if self.delta == "rounded":
+                d = round_bf16(d)
+            contrib = self._conv(d, self.w[l], s)
+            z_old = self.z[l] if self.z is not None else np.zeros_like(contrib)
+            z_new = z_old + contrib
+            if self.z32:
+                z_new = z_new.astype(np.float32).astype(np.float64)
+            y_new, y_old = self._phi(l, z_new), self._phi(l, z_old)
+            d = y_new - y_old
+            zs.append(z_new)
+            ys.append(y_new)
+        self.z = zs
+        return ys

@@ -430,3 +430,27 @@ def test_neck_recycling_equals_recompute():
     z[up] += d[up]
     ref = oracle.conv_transpose(y_new, w, 2)
     assert np.abs(z - ref).max() <= 1e-12 * np.abs(ref).max()
+
+
+def test_delta_form_model_pair_equals_recompute_and_rounding_drifts():
+    """The delta-form model: with the exact pair delta and float64 maps it
+    follows recomputation with bf16 storage (the same rounding decisions up
+    to float64 summation order, as for the loop model); rounding the delta to
+    bf16 before the scatter makes the recycled maps leave recomputation."""
+    from oracle.method_model import DeltaFormModel
+    layers = [(4, 6, 2, True), (6, 6, 1, True), (6, 4, 1, True)]
+    H, W, C0 = 14, 12, 4
+    rng = np.random.default_rng(21)
+    ws = [oracle.round_bf16(rng.standard_normal((co, ci, 3, 3)) * 0.4) for (ci, co, _, _) in layers]
+    frames = [oracle.round_bf16(f.astype(np.float64)) for f in _toy_stream(H, W, C0, 40, 8)]
+    exact = DeltaFormModel(layers, ws, delta="pair", z32=False)
+    rounded = DeltaFormModel(layers, ws, delta="rounded", z32=False)
+    worst_rounded = 0.0
+    for x in frames:
+        ys_e, ys_r = exact.step(x), rounded.step(x)
+        ref = oracle.forward(x, ws, layers, bf16_storage=True)
+        for got, r in zip(ys_e, ref):
+            assert np.abs(got - r).max() <= 1e-2 * np.abs(r).max()
+            assert (np.abs(got - r) > 1e-9 * np.abs(r).max()).mean() < 0.02
+        worst_rounded = max(worst_rounded, max(np.abs(g - r).max() / np.abs(r).max() for g, r in zip(ys_r, ref)))
+    assert worst_rounded > 1e-3
