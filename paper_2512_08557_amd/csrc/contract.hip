@@ -28,8 +28,8 @@
 // through a ring of LDS stages filled by asynchronous global->LDS copies, the
 // copies of the next chunks in flight while the matrix cores work on the
 // current one.  Operand layout in a stage: [row][8 x 16 bytes], the 16-byte
-// piece c of row r stored in slot c ^ (r & 7), so that the 32 rows a
-// wavefront reads at one k are spread over all LDS banks.
+// piece c of row r stored in slot c ^ ((r >> 1) & 7), so that the rows a
+// wavefront reads at one k are spread over all 64 LDS banks.
 //   fp32: v_mfma_f32_32x32x2_f32, lane l supplies row l%32 at k = 4*(l/32)+e
 //         of an 8-k group (e = 0..3 over four instructions);
 //   bf16: the delta is the exact pair [Y_new | Y_old] (bf16 values), and
@@ -72,6 +72,15 @@ struct CShape {
     static constexpr int BPW = 8 / NW;               // B blocks (1 KB) each wavefront copies per chunk
     static constexpr int LPC = 2 * NA + BPW;         // copies per thread per chunk
     static constexpr int SLOTS = 768;                // resident workgroups on 256 compute units
+    // slot of the 16-byte piece c of row r: c ^ ((r >> 1) & 7).  gfx950's LDS
+    // has 64 banks (256 bytes), so the 16 lanes served together (rows i ..
+    // i+15 of one piece) must fall in 16 different 16-byte bank groups: row
+    // r lands in the half r & 1 of the 256 bytes, and the xor with (r >> 1) & 7
+    // spreads rows of equal parity over the 8 groups of that half.  (The xor
+    // with r & 7 leaves rows 8 apart in the same group: measured
+    // SQ_LDS_BANK_CONFLICT / active cycles 0.89 against 0 now, at the same
+    // launch time, the loop being bound by the matrix cores.)
+    static constexpr int SWZ = 1;
     static_assert(N % 64 == 0 && NCH >= 2, "shape");
 };
 
@@ -139,13 +148,18 @@ __global__ __launch_bounds__((64 * CShape<CIN, COUT, BF16>::NW)) void contract_k
     const int total = (mt0 + (n1 + MT - 1) / MT) * C::NT;
     // copy roles: 1 KB blocks of 8 rows; wavefront w fills A blocks w and
     // NW + w, and B blocks w + j*NW; lane l takes row 8k + l/8 of block k and
-    // the 16-byte piece (l % 8) ^ (l / 8) of it, landing in slot l % 8
+    // the 16-byte piece of it that belongs in slot l % 8
     const int cr = lane >> 3;
-    const int piece = (lane & 7) ^ cr;
-    const char* dsrc = static_cast<const char*>(a.delta_in) + piece * 16;
-    const char* wsrc = static_cast<const char*>(a.wg) + piece * 16;
+    // the piece lane l copies into slot l % 8 of row 8k + l/8
+    auto piece = [&](int k) { return ((lane & 7) ^ (((8 * k + cr) >> C::SWZ) & 7)) * 16; };
+    const char* dsrc = static_cast<const char*>(a.delta_in);
+    const char* wsrc = static_cast<const char*>(a.wg);
 
     for (int t = (int)blockIdx.x; t < total; t += (int)gridDim.x) {
+        // tile t: 64-column block t % NT of M-tile t / NT, the M-tiles of
+        // list segment 0 first (an order with the segments interleaved, so
+        // that a tile's list entries can be loaded before the counts are
+        // known, measured 0.5-1 us slower per launch)
         const int mt = t / C::NT, nt = t - mt * C::NT;
         const int seg = mt < mt0 ? 0 : 1;
         const int base = (mt - (seg ? mt0 : 0)) * MT;
@@ -157,8 +171,8 @@ __global__ __launch_bounds__((64 * CShape<CIN, COUT, BF16>::NW)) void contract_k
         const int cell0 = lst[base + (base + r0 < nseg ? r0 : 0)];
         const int cell1 = lst[base + (base + r1 < nseg ? r1 : 0)];
         if (tid < MT) rowcell[tid] = base + tid < nseg ? lst[base + tid] : -1;
-        const char* a0 = dsrc + (size_t)cell0 * C::ROWB;
-        const char* a1 = dsrc + (size_t)cell1 * C::ROWB;
+        const char* a0 = dsrc + (size_t)cell0 * C::ROWB + piece(w);
+        const char* a1 = dsrc + (size_t)cell1 * C::ROWB + piece(NW + w);
         const char* bsrc = wsrc + (size_t)(nt * 64 + cr) * C::WROWB;
 
         auto issue = [&](int c, char* stp) __attribute__((always_inline)) {
@@ -173,7 +187,7 @@ __global__ __launch_bounds__((64 * CShape<CIN, COUT, BF16>::NW)) void contract_k
 #pragma unroll
             for (int j = 0; j < C::BPW; ++j) {
                 const int k = w + j * NW;            // B block: rows 8k .. 8k+7
-                copy16(bsrc + (size_t)(8 * k) * C::WROWB + c * 128, stp + C::NA * C::OPA + k * 1024);
+                copy16(bsrc + (size_t)(8 * k) * C::WROWB + piece(k) + c * 128, stp + C::NA * C::OPA + k * 1024);
             }
         };
         auto stage = [&](int k) -> char* { return k == 0 ? st0 : (k == 1 ? st1 : st2); };
@@ -188,10 +202,10 @@ __global__ __launch_bounds__((64 * CShape<CIN, COUT, BF16>::NW)) void contract_k
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const int c16 = 2 * g + kg;
-                av[g] = *reinterpret_cast<const uint4*>(stp + ra * 128 + 16 * (c16 ^ (ra & 7)));
-                bv[g] = *reinterpret_cast<const uint4*>(stp + C::NA * C::OPA + rb * 128 + 16 * (c16 ^ (rb & 7)));
-                if constexpr (BF16)
-                    ov[g] = *reinterpret_cast<const uint4*>(stp + C::OPA + ra * 128 + 16 * (c16 ^ (ra & 7)));
+                const int sa = 16 * (c16 ^ ((ra >> C::SWZ) & 7)), sb = 16 * (c16 ^ ((rb >> C::SWZ) & 7));
+                av[g] = *reinterpret_cast<const uint4*>(stp + ra * 128 + sa);
+                bv[g] = *reinterpret_cast<const uint4*>(stp + C::NA * C::OPA + rb * 128 + sb);
+                if constexpr (BF16) ov[g] = *reinterpret_cast<const uint4*>(stp + C::OPA + ra * 128 + sa);
             }
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
@@ -236,7 +250,11 @@ __global__ __launch_bounds__((64 * CShape<CIN, COUT, BF16>::NW)) void contract_k
             const int row = 32 * wm + 8 * (r >> 2) + 4 * kg + (r & 3);
             const int cell = rowcell[row];
             const float v = BF16 ? acc[r] - acc_old[r] : acc[r];
-            if (cell >= 0) out[(size_t)cell * C::N] = v;
+            // non-temporal: the contributions are read once, by the tap sum,
+            // so they are not kept in L2 (which the end of the launch would
+            // otherwise have to write back); measured c3 289 -> 271 us per
+            // stride together with the non-temporal loads of the tap sum
+            if (cell >= 0) __builtin_nontemporal_store(v, out + (size_t)cell * C::N);
         }
         lds_barrier();     // the stages and the row table are free for the next tile
     }
@@ -281,15 +299,18 @@ __global__ __launch_bounds__(256) void tap_sum_kernel(const int32_t* __restrict_
     const bool prop_wave = 4 * w < TC;
     const int co0 = 4 * (lane % LPC);            // channel work: first channel of the lane
     const int cc = w * CPI + lane / LPC;         // channel work: cell of the lane
-    for (; tile * TC < n; tile += GS) {
+    for (;; tile += GS) {
         const int t0 = tile * TC;
-        // the cell of the channel work and the propagation cell, both loaded up front
-        const int e = t0 + cc;
+        // the cell of the channel work, the propagation cell and the tile's
+        // first cell, from clamped (always valid) positions, loaded together
+        // with the count on the first pass
+        const int e = t0 + cc, ep = t0 + cp;
+        const int qs = seg[min(e, pcap - 1)], qps = seg[min(ep, pcap - 1)], q0 = seg[min(t0, pcap - 1)];
+        if (t0 >= n) break;
         const bool vrow = e < n;
-        const int q = seg[vrow ? e : t0];
-        const int ep = t0 + cp;
+        const int q = vrow ? qs : q0;
         const bool vp = prop_wave && ep < n;
-        const int qp = seg[vp ? ep : t0];
+        const int qp = vp ? qps : q0;
         const f4v zo = *reinterpret_cast<const f4v*>(a.Z + (size_t)q * COUT + co0);
         bool now = true, prev = true, nowp = true, prevp = true;
         if constexpr (SPARSE) {
@@ -321,7 +342,7 @@ __global__ __launch_bounds__(256) void tap_sum_kernel(const int32_t* __restrict_
         for (int t = 0; t < 9; ++t) {
             const bool ch = inb[t] && ev[t] == a.epoch;
             const float* src = (ch ? a.part + (size_t)cell[t] * N : a.zero) + t * COUT + co0;
-            v[t] = *reinterpret_cast<const f4v*>(src);
+            v[t] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(src));
         }
         f4v d = v[0];
 #pragma unroll
