@@ -46,3 +46,41 @@ def test_stack_strides_offsets_every_image():
     st = bench.stack_strides([a, b], H, W)
     np.testing.assert_array_equal(st.idx, [0, 34, 35 + 5])
     assert st.feats.shape == (3, 4) and st.feats[2, 0] == 2.0 and st.idx.dtype == np.int32
+
+
+def test_kernel_names_of_the_two_launch_layers():
+    """c3: the 128- and 256-channel stride-1 layers after the first run as a
+    contraction launch plus a tap sum; every other layer keeps one launch."""
+    wl = S.workload("c3")
+    L = len(wl.layers)
+    names = [bench.kernel_name(1 + l, wl) for l in range(1, L + 1)]
+    assert names[0] == "layer_kernel<64,64,2,f32>"
+    assert names[4] == "layer_kernel<64,128,2,f32>"
+    assert names[5:10] == ["tap_sum_kernel<128,f32>"] * 5
+    assert names[10] == "layer_kernel_wide<128,256,2,f32>"
+    assert names[11:] == ["tap_sum_kernel<256,f32>"] * 5
+    split = [l for l in range(1, L + 1) if bench.layer_split(l, wl)]
+    assert split == list(range(6, 11)) + list(range(12, 17))
+    assert bench.kernel_name(L + 1 + 12, wl) == "contract_kernel<256,256,f32>"
+    assert bench.launches_per_stride("contract_kernel<256,256,f32>", wl) == 5
+    assert bench.launches_per_stride("tap_sum_kernel<128,f32>", wl) == 5
+    assert bench.launches_per_stride("layer_kernel<64,64,1,f32>", wl) == 3
+    assert not any(bench.layer_split(l, S.workload("c2")) for l in range(1, 5))
+
+
+def test_block_times_split_at_stride_two_layers():
+    wl = S.workload("c3")
+    L = len(wl.layers)
+    K = 2
+    ms = [0.0] * (2 * L + 2)
+    ms[0], ms[1] = 0.010, 0.004                       # detection, ms over K strides
+    for l in range(1, L + 1):
+        ms[1 + l] = 0.001 * l                         # layer (or tap sum) l
+        if bench.layer_split(l, wl):
+            ms[L + 1 + l] = 0.002                     # its contraction launch
+    b = bench.block_times(wl, ms, K)
+    assert b["detect"] == pytest.approx(7.0)
+    assert b["block 1"] == pytest.approx(sum(0.001 * l for l in range(1, 5)) / K * 1e3)
+    assert b["block 2"] == pytest.approx((sum(0.001 * l for l in range(5, 11)) + 5 * 0.002) / K * 1e3)
+    assert b["block 3"] == pytest.approx((sum(0.001 * l for l in range(11, 17)) + 5 * 0.002) / K * 1e3)
+    assert b["all blocks"] == pytest.approx(b["block 1"] + b["block 2"] + b["block 3"])
