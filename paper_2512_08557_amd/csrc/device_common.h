@@ -245,6 +245,52 @@ __device__ __forceinline__ void epilogue4(const LayerArgs& a, int q, int co0, co
     }
 }
 
+// ---- rings of LDS stages filled by asynchronous global->LDS copies ----
+
+// s_waitcnt with only the vector-memory count limited to n.
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+    static_assert(n >= 0 && n < 64, "vmcnt");
+    __builtin_amdgcn_s_waitcnt((n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14));
+}
+
+// Workgroup barrier without a memory fence.  __syncthreads() also drains
+// every outstanding global access and LDS copy (vmcnt(0)), which would wait
+// for the copies of the later chunks too.  Here each thread first waits for
+// its own copies of the chunk it needs (wait_vm), and its LDS reads of the
+// previous chunk have completed before their matrix instructions ran, so the
+// hardware barrier makes the stage safe once this wavefront's own LDS reads
+// have completed; the empty asm statements keep the compiler from moving
+// memory accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("" ::: "memory");
+    // this wavefront's LDS reads are complete (lgkmcnt(0), no vmcnt limit)
+    __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (0 << 8) | (3 << 14));
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+// wait_vm for a count known once the chunk loop is unrolled
+__device__ __forceinline__ void wait_vm_n(int n) {
+    switch (n) {
+        case 0: wait_vm<0>(); break;
+        case 4: wait_vm<4>(); break;
+        case 6: wait_vm<6>(); break;
+        case 8: wait_vm<8>(); break;
+        case 12: wait_vm<12>(); break;
+        case 16: wait_vm<16>(); break;
+        case 18: wait_vm<18>(); break;
+        case 24: wait_vm<24>(); break;
+        case 32: wait_vm<32>(); break;
+        default: wait_vm<0>(); break;
+    }
+}
+
+__device__ __forceinline__ void copy16(const void* src, void* lds) {
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                     (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
 __device__ __forceinline__ void flag_error(int32_t* err, int bit) {
     *(volatile int32_t*)err = bit;
 }
