@@ -47,6 +47,9 @@ import streams as S  # noqa: E402
 PEAK_TFLOPS = {"f32": 157.3, "bf16": 2500.0}   # dense MFMA peaks of MI355X
 PEAK_HBM_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.txt")
+# change detection through sscater_step_sorted (one launch; the synthetic
+# pillar lists are in row-major cell order), or sscater_step with --two-pass
+SORTED = True
 METRIC = "ms per stride and changed-cell conv updates/s; fraction of HBM/MFMA roofline"
 PAPER_CONTEXT = {
     "hardware": "NVIDIA Jetson AGX Orin 32 GB (2048 Ampere cores) and AGX Xavier; real drone LiDAR, 504x504 grid",
@@ -102,7 +105,9 @@ def kernel_name(slot: int, wl, ups=(), points=False) -> str:
     upsamplers, then L + 1 + n_ups + l the contraction launch of layer l."""
     L, nu = len(wl.layers), len(ups)
     if slot == 0:
-        return "pillar_update_kernel" if points else "detect_kernel<present>"
+        if points:
+            return "pillar_update_kernel"
+        return "detect_sorted_kernel" if SORTED else "detect_kernel<present>"
     if slot == 1:
         return f"pfn_kernel<{wl.dtype}>" if points else "detect_kernel<vanished>"
     if slot >= L + 2 + nu:
@@ -330,6 +335,8 @@ def short_kernel(name: str) -> str:
     fn, _, targs = base.partition("<")
     t = [x.strip() for x in targs.rstrip(">").split(",")]
     dt = lambda v: "bf16" if v == "true" else "f32"
+    if fn == "detect_sorted_kernel" and len(t) == 3:
+        return f"detect_sorted_kernel<{t[0]},{dt(t[1])}>"
     if fn == "detect_kernel" and len(t) in (3, 4):
         return f"detect_kernel<{t[0]},{dt(t[1])},{'vanished' if t[2] == 'true' else 'present'}>"
     if fn in ("layer_kernel", "layer_kernel_wide") and len(t) in (4, 5):
@@ -344,7 +351,7 @@ def short_kernel(name: str) -> str:
 
 
 def launches_per_stride(kernel: str, wl) -> int:
-    if kernel.startswith(("detect_kernel", "pillar_update_kernel", "pfn_kernel")):
+    if kernel.startswith(("detect_kernel", "detect_sorted_kernel", "pillar_update_kernel", "pfn_kernel")):
         return 1
     L = len(wl.layers)
     names = [kernel_name(1 + l, wl) for l in range(1, L + 1)]
@@ -599,7 +606,7 @@ def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool, batch
     def run_range(lo, hi):
         for k in range(lo, hi):
             for i in range(len(engs)):
-                engs[i].step(*devs[i][k], stream=hs[i])
+                engs[i].step(*devs[i][k], stream=hs[i], sorted=SORTED)
 
     run_range(0, 1 + W)
     torch.cuda.synchronize()
@@ -682,6 +689,7 @@ def run_streams(wl, ws, K: int, W: int, n: int, cpu_seconds, no_cpu: bool, batch
             "ms_per_step": wall_ms / K, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
             "dtype": wl.dtype, "data": "synthetic",
             "config": {"workload": f"{wl.name}: {wl.description}", "grid": f"{wl.W}x{wl.H}", "C0": wl.C0,
+                       "detection": "one launch (sorted pillar lists)" if SORTED else "two passes",
                        "streams": n, "batched": batched, "layers": [f"{l.cin}->{l.cout} s{l.stride}" for l in wl.layers],
                        "strides": "a stride is one step of every stream; full window + warmup untimed",
                        "mean_active_per_stream": [sum(x[l] for x in act) / (K * n) for l in range(L + 1)]},
@@ -710,12 +718,12 @@ def run_sweep(K: int, W: int, n_full: int) -> dict:
             eng = Engine(wl.H, wl.W, wl.C0, layers_of(wl), S.weights(wl.name), dtype=wl.dtype,
                          max_pillars=wl.max_pillars)
             for k in range(1 + W):
-                eng.step(*dev[k])
+                eng.step(*dev[k], sorted=SORTED)
             torch.cuda.synchronize()
             before = eng.stats()
             t0 = time.perf_counter()
             for k in range(1 + W, 1 + W + K):
-                eng.step(*dev[k])
+                eng.step(*dev[k], sorted=SORTED)
             torch.cuda.synchronize()
             wall_ms = (time.perf_counter() - t0) * 1e3
             after = eng.stats()
@@ -725,11 +733,11 @@ def run_sweep(K: int, W: int, n_full: int) -> dict:
             # per-kernel pass over the same strides
             eng.reset()
             for k in range(1 + W):
-                eng.step(*dev[k])
+                eng.step(*dev[k], sorted=SORTED)
             eng.profile_read()
             eng.profile(True)
             for k in range(1 + W, 1 + W + K):
-                eng.step(*dev[k])
+                eng.step(*dev[k], sorted=SORTED)
             ms, cnt = eng.profile_read()
             eng.profile(False)
             # full recompute of n_full windows spread over the timed range
@@ -740,7 +748,7 @@ def run_sweep(K: int, W: int, n_full: int) -> dict:
                 a = torch.cuda.Event(enable_timing=True)
                 b = torch.cuda.Event(enable_timing=True)
                 a.record(stream)
-                eng.step(*dev[k])
+                eng.step(*dev[k], sorted=SORTED)
                 b.record(stream)
                 torch.cuda.synchronize()
                 full.append(a.elapsed_time(b))
@@ -778,6 +786,9 @@ def main() -> int:
     ap.add_argument("--no-full", action="store_true", help="skip the GPU full-recompute timing")
     ap.add_argument("--no-dense", action="store_true",
                     help="skip the context timing of the same layers recomputed densely by torch conv2d")
+    ap.add_argument("--two-pass", action="store_true",
+                    help="detect changes with the two passes of sscater_step instead of the one launch of "
+                         "sscater_step_sorted (the synthetic pillar lists are sorted by cell)")
     ap.add_argument("--neck", action="store_true", help="include the upsampling neck (c3, c4)")
     ap.add_argument("--streams", type=int, default=0,
                     help="independent streams advanced together (default: 4 for c5, else 1)")
@@ -794,6 +805,8 @@ def main() -> int:
                     help="average every counter of a rocprofv3 --pmc csv over the timed launches of --kernel and exit")
     ap.add_argument("--kernel", default="layer_kernel<64,64,1,f32>", help="kernel of --digest-pmc / --digest-counters")
     args = ap.parse_args()
+    global SORTED
+    SORTED = not args.two_pass
 
     if args.digest_trace:
         if args.sweep:
@@ -864,7 +877,7 @@ def main() -> int:
                      ups=[(u.src, u.cout, u.stride, u.relu) for u in neck],
                      up_weights=S.neck_weights(wl.name) if neck else (),
                      submanifold=sub if any(sub) else None)
-        step = lambda k: eng.step(*dev[k])
+        step = lambda k: eng.step(*dev[k], sorted=SORTED)
     L = len(wl.layers)
 
     def run_range(lo, hi):
@@ -1013,7 +1026,7 @@ def main() -> int:
         last_pts = torch.cat(dev[first + W + K - spec.window:first + W + K]).contiguous()
         full_step = lambda: eng.step_points(last_pts)
     else:
-        full_step = lambda: eng.step(*dev[W + K])
+        full_step = lambda: eng.step(*dev[W + K], sorted=SORTED)
     for _ in range(0 if args.no_full else 5):
         eng.reset()
         torch.cuda.synchronize()
@@ -1066,6 +1079,7 @@ def main() -> int:
         "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": wl.dtype, "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.description}", "grid": f"{wl.W}x{wl.H}", "C0": wl.C0,
+                   "detection": "one launch (sorted pillar lists)" if SORTED else "two passes",
                    "layers": [f"{l.cin}->{l.cout} s{l.stride}{' relu' if l.relu else ''}"
                               f"{' submanifold' if l.sub else (' sparse' if any(x.sub for x in wl.layers) else '')}"
                               for l in wl.layers],

@@ -43,8 +43,9 @@
  *
  * Errors: every call returns 0 or a negative SSCATER_E_* code, never throws.
  * Device-side input faults (a cell index outside the grid, a duplicate
- * index within one stride, or in points mode a pillar over its point
- * capacity) set a sticky flag reported as SSCATER_E_DEVICE by
+ * index within one stride, a list passed as sorted that does not increase,
+ * or in points mode a pillar over its point capacity) set a sticky flag
+ * reported as SSCATER_E_DEVICE by
  * the next call that finds it set after the offending stride has executed;
  * sscater_reset clears it.
  */
@@ -241,6 +242,18 @@ int sscater_create_sparse(const sscater_grid* grid, const sscater_layer* layers,
  * pass.  A stride whose input equals the previous one bit for bit changes
  * nothing.  Asynchronous on `stream`. */
 int sscater_step(sscater_t h, const sscater_pillars* pillars, void* stream);
+
+/* sscater_step for a pillar list whose cell indices increase strictly (the
+ * row-major order a pillar scatter produces).  Same results as sscater_step;
+ * the change detection of Alg. 1 (which cells gained, lost or changed a
+ * pillar against the previous stride) then runs as one launch that merges
+ * the new list with the previous one stretch by stretch, instead of a pass
+ * over each list.  A stride whose new list is empty or more than four times
+ * shorter than the previous one, or that follows a dense stride, takes the
+ * two passes.  A list that does not increase is a device-side input fault
+ * (SSCATER_E_DEVICE; the stride's results are then undefined).  Dense mode
+ * (idx NULL) is accepted and behaves as in sscater_step.  Asynchronous. */
+int sscater_step_sorted(sscater_t h, const sscater_pillars* pillars, void* stream);
 
 /* Write layer `layer`'s output map into dst (device, NHWC, grid dtype): the
  * maps the method keeps between passes and updates in place (Sec. III-D: the

@@ -543,7 +543,8 @@ int sscater_create_batched(const sscater_grid* grid, int32_t batch, const sscate
     return create_impl(grid, batch, layers, n_layers, weights, nullptr, 0, nullptr, out);
 }
 
-int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
+// sorted: the caller's cell indices increase strictly (sscater_step_sorted)
+static int step_impl(sscater_t h, const sscater_pillars* pl, void* stream, bool sorted) {
     if (!h || !pl || h->pfn) return SSCATER_E_INVALID_ARG;
     if (int rc = check_sticky(h)) return rc;
     const long long cells = (long long)h->cells_of(0);
@@ -587,13 +588,29 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
         const LayerState& l1 = h->layers[0];
         d.memb = MembTarget{l1.memb, l1.spec.stride, l1.Hout, l1.Wout};
     }
-    hipError_t e = timed_launch(h, 0, s, [&](const LaunchCtx& c) { return launch_detect_present(d, h->row_bytes, h->bf16, c); });
+    // Sorted lists: one launch that merges the new list with the previous
+    // one (stretch by stretch).  Its workgroups each handle the previous
+    // list's cells between two stretches of the new one, so a stride that
+    // loses most of its pillars at once (the previous list more than four
+    // times the new one, or an empty new list) and a previous dense stride
+    // take the two passes.
+    const bool one_launch = sorted && !dense && !h->prev_dense && pl->count > 0 &&
+                            (long long)h->prev_count <= 4LL * pl->count;
+    hipError_t e = hipSuccess;
+    if (one_launch) {
+        DetectArgs m = d;
+        m.prev = h->prev[h->prev_slot];
+        m.prev_count = h->prev_count;
+        e = timed_launch(h, 0, s, [&](const LaunchCtx& c) { return launch_detect_sorted(m, h->row_bytes, h->bf16, c); });
+    } else {
+        e = timed_launch(h, 0, s, [&](const LaunchCtx& c) { return launch_detect_present(d, h->row_bytes, h->bf16, c); });
+    }
     if (e != hipSuccess) return hip_fail(e);
 
     // vanished cells of the previous list, and the ownership check of the
     // new list's presence words (pillar mode only: dense input has no
     // duplicates)
-    if (!dense && (h->prev_dense || h->prev_count > 0 || pl->count > 0)) {
+    if (!one_launch && !dense && (h->prev_dense || h->prev_count > 0 || pl->count > 0)) {
         DetectArgs v = d;
         v.prev = h->prev_dense ? nullptr : h->prev[h->prev_slot];
         v.count = h->prev_dense ? (int32_t)cells : h->prev_count;
@@ -621,6 +638,12 @@ int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) {
     h->steps += 1;
     h->last_pillars = pl->count;
     return SSCATER_OK;
+}
+
+int sscater_step(sscater_t h, const sscater_pillars* pl, void* stream) { return step_impl(h, pl, stream, false); }
+
+int sscater_step_sorted(sscater_t h, const sscater_pillars* pl, void* stream) {
+    return step_impl(h, pl, stream, true);
 }
 
 int sscater_create_pfn(const sscater_grid* grid, const sscater_layer* layers, int32_t n_layers,

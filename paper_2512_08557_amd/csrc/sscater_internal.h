@@ -60,7 +60,8 @@ struct DetectArgs {
     const int32_t* idx;   // pillar cell indices (nullptr: dense mode, cell = i)
     const void* feats;    // pillar feature rows (present mode)
     int32_t count;        // rows to examine
-    const int32_t* prev;  // previous stride's cell list (vanish mode; nullptr: all cells)
+    const int32_t* prev;  // previous stride's cell list (vanish and sorted modes; nullptr: all cells)
+    int32_t prev_count;   // its length (sorted mode)
     int32_t* prev_out;    // copy of this stride's cell list (present mode, may be nullptr)
     void* X;              // persistent canvas [H0*W0][row bytes]
     uint64_t* pres;       // presence words [H0*W0]: (epoch << 32) | row of the pillar in this stride's list
@@ -189,7 +190,8 @@ struct PfnArgs {
     PropTarget next;
 };
 
-enum ErrBits { ERR_INDEX_RANGE = 1, ERR_DUPLICATE = 2, ERR_PILLAR_FULL = 4 };
+// ERR_UNSORTED: a list passed as sorted does not increase.
+enum ErrBits { ERR_INDEX_RANGE = 1, ERR_DUPLICATE = 2, ERR_PILLAR_FULL = 4, ERR_UNSORTED = 8 };
 
 // What a layer's change list is made of, for the device-side list: the cells
 // q of the layer's grid with stamp[q] == epoch, restricted for a sparse layer
@@ -226,6 +228,7 @@ inline hipError_t launch_kernel(const LaunchCtx& c, K kernel, dim3 grid, dim3 bl
 // Host-side launchers (defined in the kernel translation units).
 hipError_t launch_detect_present(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c);
 hipError_t launch_detect_vanished(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c);
+hipError_t launch_detect_sorted(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c);
 bool layer_supported(int cin, int cout, int stride, bool bf16);
 hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool bf16, bool sparse, int grid,
                         const LaunchCtx& c);

@@ -24,7 +24,7 @@ F32, BF16 = 0, 1
 
 # every function declared in include/sscater.h
 EXPORTS = ("sscater_create", "sscater_create_neck", "sscater_create_pfn", "sscater_create_sparse",
-           "sscater_create_batched", "sscater_step",
+           "sscater_create_batched", "sscater_step", "sscater_step_sorted",
            "sscater_step_points",
            "sscater_read", "sscater_reset", "sscater_destroy", "sscater_changed", "sscater_changed_noalloc",
            "sscater_stats", "sscater_profile", "sscater_profile_read", "sscater_strerror")
@@ -92,6 +92,7 @@ def lib() -> ctypes.CDLL:
         L.sscater_create_batched.argtypes = [ctypes.POINTER(Grid), i32, ctypes.POINTER(Layer), i32,
                                              ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(vp)]
         L.sscater_step.argtypes = [vp, ctypes.POINTER(Pillars), vp]
+        L.sscater_step_sorted.argtypes = [vp, ctypes.POINTER(Pillars), vp]
         L.sscater_step_points.argtypes = [vp, vp, i32, vp]
         L.sscater_read.argtypes = [vp, i32, vp, ctypes.c_size_t, vp]
         L.sscater_reset.argtypes = [vp, vp]
@@ -234,10 +235,11 @@ class Engine:
         return self._torch.float32 if self.dtype == "f32" else self._torch.bfloat16
 
     # -- C ABI calls -------------------------------------------------------------
-    def step(self, idx, feats, stream=None) -> None:
+    def step(self, idx, feats, stream=None, sorted=False) -> None:
         """idx: int32 cuda tensor [P] (or None for a dense [H, W, C0] canvas);
         feats: cuda tensor [P, C0] of the grid dtype (float32, or bf16 bits as
-        int16/uint16/bfloat16)."""
+        int16/uint16/bfloat16).  sorted: idx increases strictly
+        (sscater_step_sorted)."""
         if idx is not None:
             if idx.dtype != self._torch.int32 or not idx.is_cuda or not idx.is_contiguous():
                 raise ValueError("idx must be a contiguous int32 cuda tensor")
@@ -248,8 +250,9 @@ class Engine:
                       (4 if self.dtype == "f32" else 2) or feats.numel() != count * self.C0):
             raise ValueError("feats must be a contiguous cuda tensor [count, C0] of the grid dtype")
         p = Pillars(idx.data_ptr() if idx is not None else None, feats.data_ptr() if count else None, count)
-        _check(lib().sscater_step(self._h, ctypes.byref(p), self._stream(stream, (idx, feats if count else None))),
-               "sscater_step")
+        fn = lib().sscater_step_sorted if sorted else lib().sscater_step
+        _check(fn(self._h, ctypes.byref(p), self._stream(stream, (idx, feats if count else None))),
+               "sscater_step_sorted" if sorted else "sscater_step")
 
     def step_points(self, points, stream=None) -> None:
         """points: contiguous float32 cuda tensor [n, 4] = (x, y, z, intensity)

@@ -84,7 +84,7 @@ def oracle_maps(stride, wl, ws):
     return oracle.forward(x, ws, layers_of(wl), bf16_storage=(wl.dtype == "bf16"))
 
 
-def run_stream(name, n_strides=None, map_every=10, list_every=1):
+def run_stream(name, n_strides=None, map_every=10, list_every=1, sorted=False):
     wl = S.workload(name)
     ws = S.weights(name)
     strides = S.make_stream(name, n_strides=n_strides)
@@ -96,7 +96,7 @@ def run_stream(name, n_strides=None, map_every=10, list_every=1):
     worst = [0.0] * len(wl.layers)
     for t, (st, (idx, feats)) in enumerate(zip(strides, dev)):
         note(f"[gpu-test] {name} stride {t} P={len(st.idx)}")
-        eng.step(idx, feats)
+        eng.step(idx, feats, sorted=sorted)
         bits = canvas_bits(st, wl)
         if t % list_every == 0 or t == last:
             ref_lists = oracle.changed_lists(prev_bits, bits, strides_l)

@@ -31,7 +31,7 @@ def _engine(H, W, C0, layers, ws, sub, dtype, max_pillars):
     return Engine(H, W, C0, layers, ws, dtype=dtype, max_pillars=max_pillars, submanifold=sub)
 
 
-def _run(name, n_strides, map_every):
+def _run(name, n_strides, map_every, sorted=False):
     wl = S.workload(name)
     ws = S.weights(name)
     layers = [(l.cin, l.cout, l.stride, bool(l.relu)) for l in wl.layers]
@@ -42,7 +42,7 @@ def _run(name, n_strides, map_every):
     prev_occ = np.zeros((wl.H, wl.W), bool)
     for t, st in enumerate(strides):
         note(f"[gpu-test] {name} stride {t} P={len(st.idx)}")
-        eng.step(*to_device(st, wl.dtype))
+        eng.step(*to_device(st, wl.dtype), sorted=sorted)
         bits = canvas_bits(st, wl)
         occ = SP.occupancy(st.idx, wl.H, wl.W)
         check_lists(eng, SP.changed_lists(prev_bits, bits, prev_occ, occ, layers, sub), f"{name} stride {t}")
@@ -75,10 +75,17 @@ STACKS = [
 ]
 
 
-@pytest.mark.parametrize("H,W,C0,layers,sub,dtype", STACKS)
-def test_random_sparse_stacks_with_toggles_and_zero_pillars(H, W, C0, layers, sub, dtype):
+def test_s2_sorted_pillar_lists_40_strides():
+    """The one-launch detection of sorted lists (sscater_step_sorted)."""
+    _run("s2", 40, 20, sorted=True)
+
+
+@pytest.mark.parametrize("H,W,C0,layers,sub,dtype,order",
+                         [st + ("shuffled",) for st in STACKS] + [st + ("sorted",) for st in STACKS[:2]])
+def test_random_sparse_stacks_with_toggles_and_zero_pillars(H, W, C0, layers, sub, dtype, order):
     """Pillars appear and vanish every stride, some pillars carry all-zero
-    features (active sites holding zeros), the pillar order is shuffled."""
+    features (active sites holding zeros), the pillar order is shuffled (or
+    sorted, through sscater_step_sorted)."""
     rng = np.random.default_rng(H * 100 + W)
     ws = []
     for (ci, co, _s, _r) in layers:
@@ -103,7 +110,9 @@ def test_random_sparse_stacks_with_toggles_and_zero_pillars(H, W, C0, layers, su
         zero = occ & (rng.random(H * W) < 0.05)            # present pillars with all-zero features
         feat[zero] = 0.0
         idx = np.flatnonzero(occ).astype(np.int32)
-        idx = idx[rng.permutation(len(idx))]
+        perm = rng.permutation(len(idx))
+        if order == "shuffled":
+            idx = idx[perm]
         f = feat[idx]
         if dtype == "bf16":
             fb = S.round_to_bf16_bits(f).reshape(f.shape)
@@ -111,7 +120,7 @@ def test_random_sparse_stacks_with_toggles_and_zero_pillars(H, W, C0, layers, su
             st = S.Stride(t, idx, fb)
         else:
             st = S.Stride(t, idx, f.copy())
-        eng.step(*to_device(st, dtype))
+        eng.step(*to_device(st, dtype), sorted=(order == "sorted"))
         canvas = S.canvas(st, H, W, C0)
         bits = oracle.canvas_bits(canvas, dtype)
         occ2 = occ.reshape(H, W).copy()
