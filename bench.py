@@ -263,6 +263,7 @@ KERNEL_FILES = {
     "contract_kernel": ("contract.hip", "device_common.h", "sscater_internal.h"),
     "tap_sum_kernel": ("contract.hip", "device_common.h", "sscater_internal.h"),
     "detect_kernel": ("detect.hip", "device_common.h", "sscater_internal.h"),
+    "detect_sorted_kernel": ("detect.hip", "device_common.h", "sscater_internal.h"),
     "upsample_kernel": ("upsample.hip", "device_common.h", "sscater_internal.h"),
     "pfn_kernel": ("pfn.hip", "device_common.h", "sscater_internal.h"),
     "pillar_update_kernel": ("pfn.hip", "device_common.h", "sscater_internal.h"),
