@@ -89,6 +89,8 @@ def test_calls_reject_null_handle():
     lib = ssc.lib()
     p = E.Pillars(None, None, 0)
     assert lib.sscater_step(None, ctypes.byref(p), None) == ssc.E_INVALID_ARG
+    assert lib.sscater_step_sorted(None, ctypes.byref(p), None) == ssc.E_INVALID_ARG
+    assert lib.sscater_step_sorted(None, None, None) == ssc.E_INVALID_ARG
     assert lib.sscater_read(None, 0, None, 0, None) == ssc.E_INVALID_ARG
     assert lib.sscater_reset(None, None) == ssc.E_INVALID_ARG
     assert lib.sscater_destroy(None) == ssc.E_INVALID_ARG
