@@ -247,12 +247,12 @@ int sscater_step(sscater_t h, const sscater_pillars* pillars, void* stream);
  * row-major order a pillar scatter produces).  Same results as sscater_step;
  * the change detection of Alg. 1 (which cells gained, lost or changed a
  * pillar against the previous stride) then runs as one launch that merges
- * the new list with the previous one stretch by stretch, instead of a pass
- * over each list.  A stride whose new list is empty or more than four times
- * shorter than the previous one, or that follows a dense stride, takes the
- * two passes.  A list that does not increase is a device-side input fault
- * (SSCATER_E_DEVICE; the stride's results are then undefined).  Dense mode
- * (idx NULL) is accepted and behaves as in sscater_step.  Asynchronous. */
+ * the new list with the previous one chunk by chunk, instead of a pass over
+ * each list.  A stride that follows a dense stride or an sscater_step call
+ * (whose list may come in any order) takes the two passes.  A list that does
+ * not increase is a device-side input fault (SSCATER_E_DEVICE; the stride's
+ * results are then undefined).  Dense mode (idx NULL) is accepted and
+ * behaves as in sscater_step.  Asynchronous. */
 int sscater_step_sorted(sscater_t h, const sscater_pillars* pillars, void* stream);
 
 /* Write layer `layer`'s output map into dst (device, NHWC, grid dtype): the

@@ -102,6 +102,7 @@ struct sscater {
     int prev_slot = 0;
     int32_t prev_count = 0;
     bool prev_dense = false;
+    bool prev_sorted = true;       // the previous list is known to increase (or is empty)
     int32_t* counters = nullptr;   // [2][2*(L+1)][NSHARD][CSTRIDE]: per set cnt[0..L][shard], pairs[0..L][shard]
     long long* cum = nullptr;      // running totals, same layout as one set
     int32_t* err_host = nullptr;   // host-visible sticky error word
@@ -589,13 +590,11 @@ static int step_impl(sscater_t h, const sscater_pillars* pl, void* stream, bool 
         d.memb = MembTarget{l1.memb, l1.spec.stride, l1.Hout, l1.Wout};
     }
     // Sorted lists: one launch that merges the new list with the previous
-    // one (stretch by stretch).  Its workgroups each handle the previous
-    // list's cells between two stretches of the new one, so a stride that
-    // loses most of its pillars at once (the previous list more than four
-    // times the new one, or an empty new list) and a previous dense stride
-    // take the two passes.
-    const bool one_launch = sorted && !dense && !h->prev_dense && pl->count > 0 &&
-                            (long long)h->prev_count <= 4LL * pl->count;
+    // one chunk by chunk; it needs the previous list sorted too, so a stride
+    // after a dense one or after an sscater_step (whose list may come in any
+    // order) takes the two passes, which then check the order of this one.
+    d.sorted = sorted && !dense ? 1 : 0;
+    const bool one_launch = sorted && !dense && !h->prev_dense && h->prev_sorted;
     hipError_t e = hipSuccess;
     if (one_launch) {
         DetectArgs m = d;
@@ -629,6 +628,7 @@ static int step_impl(sscater_t h, const sscater_pillars* pl, void* stream, bool 
         h->prev_slot = cur_slot;
         h->prev_count = pl->count;
         h->prev_dense = false;
+        h->prev_sorted = sorted;
     } else {
         h->prev_count = 0;
         h->prev_dense = true;
@@ -873,6 +873,7 @@ int sscater_reset(sscater_t h, void* stream) {
     ++h->epoch;   // every stamp becomes stale
     h->prev_count = 0;
     h->prev_dense = false;
+    h->prev_sorted = true;
     h->last_set = -1;
     h->steps = 0;
     h->last_pillars = 0;

@@ -74,10 +74,10 @@ __device__ __forceinline__ void emit_rows(const DetectArgs& a, int p, int pc, bo
     prop_finish<G>(a.next, a.epoch, shard, pb);
 }
 
-// Row i of the new list (present pass), valid while i < iend.  ORDER: the
-// list must increase strictly (the one-launch form for sorted lists); a row
-// not above its predecessor is an input fault.
-template <int ROWB, bool BF16, bool SPARSE, bool ORDER>
+// Row i of the new list (present pass), valid while i < iend.  a.sorted: the
+// list was passed as increasing strictly; a row not above its predecessor is
+// an input fault.
+template <int ROWB, bool BF16, bool SPARSE>
 __device__ __forceinline__ void present_rows(const DetectArgs& a, int i, int iend, int shard) {
     constexpr int G = ROWB / 16;
     const int sub = lane_id() % G;
@@ -90,7 +90,7 @@ __device__ __forceinline__ void present_rows(const DetectArgs& a, int i, int ien
             act = false;
         }
     }
-    if constexpr (ORDER) {
+    if (a.sorted) {
         // the next row's cell, from a clamped position, in the same round trip
         const int nx = a.idx[min(i + 1, a.count - 1)];
         if (act && sub == 0 && i + 1 < a.count && nx <= p) flag_error(a.err, nx == p ? ERR_DUPLICATE : ERR_UNSORTED);
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
     for (int base = wave * PPW; base < rows; base += nwaves * PPW) {
         const int i = base + lane / G;
         if constexpr (!VANISH) {
-            present_rows<ROWB, BF16, SPARSE, false>(a, i, a.count, shard);
+            present_rows<ROWB, BF16, SPARSE>(a, i, a.count, shard);
         } else {
             bool act = i < a.count;
             int p = -1;
@@ -172,89 +172,124 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
     }
 }
 
+// Lower bound of x in the sorted list v[0, len) (the first position whose
+// cell is not below x), computed by the 32 lanes of one half-wavefront
+// together: each round loads 32 evenly spaced samples of the remaining
+// stretch and keeps the stretch between the last sample below x and the
+// first one not below it, a factor 32 per round trip.  `half` masks this
+// half's lanes; both halves run the same rounds (a uniform loop), each with
+// its own x.
+__device__ __forceinline__ int lower_bound32(const int32_t* __restrict__ v, int len, int x,
+                                             unsigned long long half) {
+    const int sl = lane_id() & 31;
+    int L = 0, R = len;        // the answer is in [L, R]; entries [L, R) unchecked
+    while (__ballot(L < R) != 0ull) {
+        const int n = R - L;
+        const int step = (n + 31) / 32;
+        const int q = L + (sl + 1) * step - 1;      // sample sl: the last entry of its stretch
+        const bool valid = n > 0 && q < R;
+        const int s = v[min(max(q, 0), max(len - 1, 0))];
+        const int c = (int)__popcll(__ballot(valid && s < x) & half);   // samples below x: a prefix
+        if (n > 0) {
+            const int qc = L + (c + 1) * step - 1;  // the first sample not below x, if any
+            if (qc < R) R = qc;
+            L = L + c * step;
+        }
+    }
+    return L;
+}
+
 // Sorted pillar lists (cells strictly increasing, the row-major order of a
-// pillar scatter): both passes in one launch.  Chunk k of the new list (CH
-// rows) owns the cells [lo, hi) from its first row's cell (0 for the first
-// chunk) up to the next chunk's first cell (the grid's end for the last), so
-// the new pillars in that range are exactly the chunk's rows and a cell of
-// the previous list in the range vanished iff it is not one of them: the
-// comparison of the two lists stays inside the workgroup.  Wavefronts 0..2
-// take the chunk's rows (the present pass); wavefront 3 finds the previous
-// list's cells in [lo, hi) by a 32-way sampled search of that sorted list
-// (lanes 0-31 for lo, 32-63 for hi, a factor 32 per round trip), tests each
-// against the chunk's cells (held one per lane) and processes the vanished
-// ones.
+// pillar scatter): both passes in one launch, every comparison of the two
+// lists inside one workgroup.  Workgroup k takes rows k*CH .. of the new list
+// (the present pass, wavefronts 0..2) and entries 64k .. 64k+63 of the
+// previous list (wavefront 3): a previous cell p vanished iff the new list
+// does not hold p.  Wavefront 3 finds the stretch of the new list between its
+// first and last previous cell by a 32-way sampled search (lanes 0-31 and
+// 32-63 for the two ends), then tests each of its cells against that stretch:
+// by binary lifting over shuffles when the stretch fits the 64 lanes, else by
+// a binary search per lane (a region of new pillars between two previous
+// ones).  The vanished cells (at most 64) go to LDS and all four wavefronts
+// process them.  Each workgroup's work is bounded by its two chunks, so a
+// region that loses all its pillars at once spreads over the workgroups of
+// its stretch of the previous list.
 template <int ROWB, bool BF16, bool SPARSE>
 __global__ __launch_bounds__(256) void detect_sorted_kernel(DetectArgs a) {
     constexpr int G = ROWB / 16;
     constexpr int PPW = 64 / G;
-    constexpr int CH = 3 * PPW < 64 ? 3 * PPW : 64;   // rows of a chunk, at most one per lane of wavefront 3
-    __shared__ int vq[64];                            // wavefront 3: the vanished cells of a batch
+    constexpr int CH = 3 * PPW < 64 ? 3 * PPW : 64;   // rows of the new list per workgroup
+    __shared__ int vq[64];                            // the vanished cells of the workgroup's previous chunk
+    __shared__ int nvq;
     const int lane = lane_id();
     const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int shard = (int)(blockIdx.x % NSHARD);
     const int n = a.count, m = a.prev_count;
-    const int nchunk = max(1, (n + CH - 1) / CH);
+    const int nchunk = max(max((n + CH - 1) / CH, (m + 63) / 64), 1);
 
     if (a.zero_ptr && blockIdx.x == 0)
         for (int i = threadIdx.x; i < a.zero_n; i += blockDim.x) a.zero_ptr[i] = 0;
 
     for (int k = (int)blockIdx.x; k < nchunk; k += (int)gridDim.x) {
-        const int i0 = k * CH, i1 = min(i0 + CH, n);
         if (w < 3) {
-            if (n > 0 && w * PPW < CH) present_rows<ROWB, BF16, SPARSE, true>(a, i0 + w * PPW + lane / G, i1, shard);
-            continue;
-        }
-        // the chunk's cell range and its cells, one per lane
-        const int lo = i0 > 0 ? a.idx[i0] : 0;
-        const int hi = i1 < n ? a.idx[i1] : a.HW;
-        const int nc = i1 - i0;
-        const int cv = n > 0 ? a.idx[min(i0 + lane, n - 1)] : 0;
-        // lower bounds of lo (lanes 0-31) and hi (lanes 32-63) in the previous
-        // list: the answer stays in [L, R], the entries [L, R) unchecked
-        const int x = lane < 32 ? lo : hi;
-        const unsigned long long half = lane < 32 ? 0x00000000FFFFFFFFull : 0xFFFFFFFF00000000ull;
-        const int sl = lane & 31;
-        int L = 0, R = m;
-        while (__ballot(L < R) != 0ull) {
-            const int len = R - L;
-            const int step = (len + 31) / 32;
-            const int q = L + (sl + 1) * step - 1;       // sample sl: the last entry of its stretch
-            const bool valid = len > 0 && q < R;
-            const int v = a.prev[min(max(q, 0), m - 1)];
-            const int c = (int)__popcll(__ballot(valid && v < x) & half);   // samples below x: a prefix
-            if (len > 0) {
-                const int qc = L + (c + 1) * step - 1;   // the first sample not below x, if any
-                if (qc < R) R = qc;
-                L = L + c * step;
-            }
-        }
-        const int plo = __shfl(L, 0), phi = __shfl(L, 32);
-        for (int j0 = plo; j0 < phi; j0 += 64) {
-            const int j = j0 + lane;
-            const bool in = j < phi;
-            const int p = a.prev[min(j, m - 1)];
-            // entries of the chunk below p (binary lifting over lanes 0 .. nc-1).
-            // Every shuffle runs on the whole wavefront, outside any condition:
-            // a lane reading an inactive lane's value gets 0.
-            int pos = 0;
+            const int i0 = k * CH;
+            if (i0 < n && w * PPW < CH) present_rows<ROWB, BF16, SPARSE>(a, i0 + w * PPW + lane / G,
+                                                                              min(i0 + CH, n), shard);
+        } else {
+            const int j0 = 64 * k;
+            int nv = 0;
+            if (j0 < m) {
+                const int np = min(64, m - j0);
+                const bool in = lane < np;
+                const int p = a.prev[j0 + (in ? lane : 0)];
+                // the new list's stretch [b0, b1) of cells in [first, last] of
+                // this chunk (both ends searched at once)
+                const int first = a.prev[j0], last = a.prev[j0 + np - 1];
+                const unsigned long long half = lane < 32 ? 0x00000000FFFFFFFFull : 0xFFFFFFFF00000000ull;
+                const int L = lower_bound32(a.idx, n, lane < 32 ? first : last + 1, half);
+                const int b0 = __shfl(L, 0), b1 = __shfl(L, 32);
+                const int len = b1 - b0;
+                bool member = false;
+                if (len <= 64) {
+                    // the stretch one cell per lane; every shuffle runs on the
+                    // whole wavefront (a lane reading an inactive lane gets 0)
+                    const int cv = len > 0 ? a.idx[b0 + min(lane, len - 1)] : 0;
+                    int pos = 0;
 #pragma unroll
-            for (int b = 32; b >= 1; b >>= 1) {
-                const int v = __shfl(cv, min(pos + b - 1, 63));
-                if (pos + b <= nc && v < p) pos += b;
+                    for (int b = 32; b >= 1; b >>= 1) {
+                        const int v = __shfl(cv, min(pos + b - 1, 63));
+                        if (pos + b <= len && v < p) pos += b;
+                    }
+                    const int at = __shfl(cv, min(pos, 63));
+                    member = pos < len && at == p;
+                } else {
+                    // a long stretch: binary search per lane in the new list
+                    int lo = b0, hi = b1;
+                    while (__ballot(lo < hi) != 0ull) {
+                        const int mid = (lo + hi) >> 1;
+                        const int v = a.idx[min(mid, n - 1)];
+                        if (lo < hi) {
+                            if (v < p) lo = mid + 1;
+                            else hi = mid;
+                        }
+                    }
+                    member = lo < b1 && a.idx[min(lo, n - 1)] == p;
+                }
+                const bool van = in && p >= 0 && p < a.HW && !member;
+                const unsigned long long vm = __ballot(van);
+                if (van) vq[__popcll(vm & ((1ull << lane) - 1ull))] = p;
+                nv = (int)__popcll(vm);
             }
-            const int at = __shfl(cv, min(pos, 63));
-            const bool member = pos < nc && at == p;
-            const bool van = in && p >= 0 && p < a.HW && !member;
-            const unsigned long long vm = __ballot(van);
-            if (van) vq[__popcll(vm & ((1ull << lane) - 1ull))] = p;
-            const int nv = (int)__popcll(vm);
-            for (int r0 = 0; r0 < nv; r0 += PPW) {
-                const int r = r0 + lane / G;
-                const bool act = r < nv;
-                vanished_rows<ROWB, BF16, SPARSE>(a, vq[act ? r : 0], act, shard);
-            }
+            if (lane == 0) nvq = nv;
         }
+        // the chunk's vanished cells, PPW per wavefront pass over all four
+        __syncthreads();
+        const int nv = nvq;
+        for (int r0 = w * PPW; r0 < nv; r0 += 4 * PPW) {
+            const int r = r0 + lane / G;
+            const bool act = r < nv;
+            vanished_rows<ROWB, BF16, SPARSE>(a, vq[act ? r : 0], act, shard);
+        }
+        __syncthreads();   // vq and nvq are rewritten by the next chunk
     }
 }
 
@@ -293,7 +328,7 @@ static hipError_t launch_detect(const DetectArgs& a, int row_bytes, bool bf16, c
 hipError_t launch_detect_sorted(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c) {
     const int G = row_bytes / 16;
     const int ch = std::min(3 * (64 / G), 64);
-    long long blocks = ((long long)a.count + ch - 1) / ch;
+    long long blocks = std::max(((long long)a.count + ch - 1) / ch, ((long long)a.prev_count + 63) / 64);
     if (blocks < 1) blocks = 1;
     if (blocks > 4096) blocks = 4096;
     dim3 grid((unsigned)blocks), block(256);

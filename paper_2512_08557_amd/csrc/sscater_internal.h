@@ -62,6 +62,7 @@ struct DetectArgs {
     int32_t count;        // rows to examine
     const int32_t* prev;  // previous stride's cell list (vanish and sorted modes; nullptr: all cells)
     int32_t prev_count;   // its length (sorted mode)
+    int32_t sorted;       // the new list was passed as increasing strictly: checked in the present pass
     int32_t* prev_out;    // copy of this stride's cell list (present mode, may be nullptr)
     void* X;              // persistent canvas [H0*W0][row bytes]
     uint64_t* pres;       // presence words [H0*W0]: (epoch << 32) | row of the pillar in this stride's list

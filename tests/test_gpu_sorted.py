@@ -2,9 +2,10 @@
 (sscater_step_sorted) through the C ABI: against the CPU oracle on the
 backbone streams (lists bit for bit, maps within 1e-4 * max|ref| for fp32 and
 2e-2 for bf16), and bit for bit against the two-pass detection of
-sscater_step on random grids whose pillars appear and vanish, including the
-strides that fall back to the two passes (an empty list, a list that lost most
-of its pillars, a stride after a dense one)."""
+sscater_step on random grids whose pillars appear and vanish: regions that
+empty or fill at once (a previous chunk against a long stretch of the new
+list), an empty list, a stride after a dense one and a stride after an
+unsorted sscater_step call (both take the two passes)."""
 import numpy as np
 import pytest
 
@@ -109,21 +110,55 @@ def test_sorted_matches_two_pass_bitwise(H, W, C0, layers, dtype):
         r = rng.random(H * W) < 0.15
         feat[r] = rng.standard_normal((int(r.sum()), C0))
         stride(t, occ)
-    keep = occ & (rng.random(H * W) < 0.1)             # most pillars vanish: the two passes
+    keep = occ & (rng.random(H * W) < 0.1)             # most pillars vanish
     stride(9, keep)
-    stride(10, occ)                                    # they come back (the one launch again)
+    stride(10, occ)                                    # they come back
     stride(11, np.zeros(H * W, bool))                  # an empty list
     stride(12, occ)
     stride(13, occ, dense=True)                        # a dense stride, then the previous list is all cells
     occ = occ ^ (rng.random(H * W) < 0.1)
     stride(14, occ)
     occ = occ ^ (rng.random(H * W) < 0.1)
-    st = stride(15, occ)
+    stride(15, occ)
     stride(16, occ)                                    # nothing changed
     assert e1.stats()["active"][0] == 0
+    grid = occ.reshape(H, W).copy()
+    r0, r1 = H // 4, max(H // 4 + 1, 3 * H // 4)
+    grid[r0:r1, :] = False                             # a band empties at once
+    occ = grid.reshape(-1)
+    stride(17, occ)
+    grid[r0:r1, :] = True                              # and fills completely: a long stretch of new cells
+    occ = grid.reshape(-1)                             # between two previous ones
+    r = rng.random(H * W) < 0.5
+    feat[r] = rng.standard_normal((int(r.sum()), C0))
+    stride(18, occ)
+    occ = occ ^ (rng.random(H * W) < 0.05)
+    st = stride(19, occ)
     x = oracle.exact_canvas(S.canvas(st, H, W, C0), dtype)
     check_maps(e1, oracle.forward(x, ws, layers, bf16_storage=(dtype == "bf16")),
                1e-4 if dtype == "f32" else 2e-2, "end")
+    e1.close()
+    e2.close()
+
+
+def test_sorted_after_an_unsorted_step():
+    """A stride through sscater_step with a shuffled list, then sorted strides:
+    the first of them takes the two passes (its previous list is not
+    sorted), the next ones the one launch; all equal the two passes."""
+    wl = S.workload("c4")
+    ws = S.weights("c4")
+    strides = S.make_stream("c4", n_strides=5)
+    e1, e2 = make_engine(wl, ws), make_engine(wl, ws)
+    rng = np.random.default_rng(3)
+    for t, st in enumerate(strides):
+        idx, feats = to_device(st, wl.dtype)
+        if t == 1:
+            perm = torch.from_numpy(rng.permutation(len(st.idx))).cuda()
+            e1.step(idx[perm].contiguous(), feats[perm].contiguous())
+        else:
+            e1.step(idx, feats, sorted=True)
+        e2.step(idx, feats)
+        _same(e1, e2, len(wl.layers), f"stride {t}")
     e1.close()
     e2.close()
 
