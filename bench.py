@@ -421,7 +421,7 @@ def digest_sweep_trace(path: str, steps: int, warmup: int) -> str:
                        f"{statistics.fmean(v[span + 1 + warmup:2 * span]):.2f} | "
                        f"{statistics.fmean(v[2 * span:]):.2f} |")
     for k in sorted(by):
-        if k.startswith("detect_kernel"):
+        if k.startswith(("detect_kernel", "detect_sorted_kernel")):
             v = by[k]
             out.append(f"| all | all | {k} | {statistics.fmean(v):.2f} (every launch) | | |")
     return "\n".join(out)
