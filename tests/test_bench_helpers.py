@@ -84,3 +84,17 @@ def test_block_times_split_at_stride_two_layers():
     assert b["block 2"] == pytest.approx((sum(0.001 * l for l in range(5, 11)) + 5 * 0.002) / K * 1e3)
     assert b["block 3"] == pytest.approx((sum(0.001 * l for l in range(11, 17)) + 5 * 0.002) / K * 1e3)
     assert b["all blocks"] == pytest.approx(b["block 1"] + b["block 2"] + b["block 3"])
+
+
+def test_detection_slot_names_follow_the_detection_form(monkeypatch):
+    wl = S.workload("c3")
+    monkeypatch.setattr(bench, "SORTED", True)
+    assert bench.kernel_name(0, wl) == "detect_sorted_kernel"
+    monkeypatch.setattr(bench, "SORTED", False)
+    assert bench.kernel_name(0, wl) == "detect_kernel<present>"
+    assert bench.kernel_name(1, wl) == "detect_kernel<vanished>"
+    assert bench.short_kernel("void ssc::detect_sorted_kernel<256, false, false>(ssc::DetectArgs)") == \
+        "detect_sorted_kernel<256,f32>"
+    assert bench.short_kernel("void ssc::detect_kernel<128, true, true, false>(ssc::DetectArgs)") == \
+        "detect_kernel<128,bf16,vanished>"
+    assert bench.launches_per_stride("detect_sorted_kernel<256,f32>", wl) == 1
