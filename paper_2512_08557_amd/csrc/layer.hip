@@ -59,13 +59,21 @@ namespace ssc {
 // KS = 4 wavefronts split the contraction (the (tap, chunk) steps) and add
 // their partial sums through LDS (measured: a 2-way split at COUT = 32 is
 // slower than 2 wavefronts with the whole contraction each).
-template <int COUT>
+// A stride-2 layer with more than four blocks (cout 128 and 256) spreads
+// them over CS workgroups per tile, one block per wavefront each, on the same
+// XCD: its output list is ~4x shorter than its input list (the c3/c4 layer
+// 64->128: ~80 tiles, fewer than the compute units), so a wavefront's matrix
+// work is the chain that ends the launch.  (Stride 1 with ~170 tiles: the
+// split only doubles the gathers; measured 1 us slower per launch.)
+template <int COUT, int S = 1>
 struct LayerShape {
     static constexpr int NCBT = (COUT + 15) / 16;           // 16-wide cout blocks
-    static constexpr int NWC = NCBT >= 4 ? 4 : NCBT;        // wavefronts across the cout blocks
+    static constexpr int CS = S == 2 && NCBT > 4 ? NCBT / 4 : 1;   // workgroups per tile (cout parts)
+    static constexpr int NCBW = NCBT / CS;                  // cout blocks per workgroup
+    static constexpr int NWC = NCBW >= 4 ? 4 : NCBW;        // wavefronts across the cout blocks
     static constexpr int KS = NWC == 1 ? 4 : 1;             // wavefronts across the contraction
     static constexpr int NW = NWC * KS;                     // wavefronts per workgroup
-    static constexpr int NCB = NCBT / NWC;                  // cout blocks per wavefront
+    static constexpr int NCB = NCBW / NWC;                  // cout blocks per wavefront
 };
 
 // One 16-channel (fp32) or 32-value (bf16 pair) chunk of the contraction for
@@ -92,12 +100,14 @@ __device__ __forceinline__ void mfma_chunk(f4v (&acc)[NCB], const uint4 av, cons
 // scalar arguments: the build preloads them into SGPRs, so the list entry and
 // count loads that open every tile need not wait for the argument fetch.
 template <int CIN, int COUT, int S, bool BF16, bool SPARSE>
-__global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(const int32_t* __restrict__ plist,
+__global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(const int32_t* __restrict__ plist,
                                                                           const int32_t* __restrict__ pcount, int pcap,
                                                                           LayerArgs a) {
-    constexpr int NCBT = LayerShape<COUT>::NCBT;
-    constexpr int NCB = LayerShape<COUT>::NCB;
-    constexpr int NWC = LayerShape<COUT>::NWC, KS = LayerShape<COUT>::KS;
+    using LS = LayerShape<COUT, S>;
+    constexpr int NCBT = LS::NCBT;
+    constexpr int NCB = LS::NCB;
+    constexpr int NWC = LS::NWC, KS = LS::KS;
+    constexpr int CS = LS::CS, NCBW = LS::NCBW;
     constexpr int KTOT = BF16 ? 2 * CIN : CIN;   // contraction length per tap
     constexpr int KCH = BF16 ? 32 : 16;          // k per 64-byte chunk
     constexpr int NCH = KTOT / KCH;
@@ -107,20 +117,23 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(const 
     const int lane = (int)(threadIdx.x & 63u), wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int cl = lane & 15, g = lane >> 4;
     const int cw = wave % NWC, ks = wave / NWC;  // cout group, contraction share
-    const int G = (int)gridDim.x;                // a multiple of 32 * NSHARD
+    const int G = (int)gridDim.x;                // a multiple of 32 * NSHARD * CS
 
-    // tiles of segment (b / 8) % NSHARD, first one without waiting for the
-    // count.  The workgroups of a segment sit on all eight XCDs (workgroup b
-    // runs on XCD b % 8), so an uneven split of the list over the segments
-    // does not load one XCD more than another, and runs of 4 consecutive
-    // tiles (neighbouring cells, which share input rows) share an XCD's L2:
-    // with x = b % 8 and h = b / (8 * NSHARD), the first tile is
-    // 32 * (h / 4) + 4 * x + h % 4, a bijection onto [0, G / NSHARD).
+    // tiles of segment (b / (8 * CS)) % NSHARD, first one without waiting
+    // for the count.  The workgroups of a segment sit on all eight XCDs
+    // (workgroup b runs on XCD b % 8), so an uneven split of the list over
+    // the segments does not load one XCD more than another, and runs of 4
+    // consecutive tiles (neighbouring cells, which share input rows) share an
+    // XCD's L2: with x = b % 8, part = (b / 8) % CS and h = b / (8 * CS *
+    // NSHARD), the first tile is 32 * (h / 4) + 4 * x + h % 4, a bijection
+    // onto [0, G / (NSHARD * CS)) for each part; the parts of a tile share
+    // its XCD.
     const int b = (int)blockIdx.x;
-    const int shard = (b >> 3) % NSHARD;
-    const int GS = G / NSHARD;                   // workgroups per segment
+    const int part = (b >> 3) % CS;              // cout blocks part*NCBW .. of the tile
+    const int shard = ((b >> 3) / CS) % NSHARD;
+    const int GS = G / (NSHARD * CS);            // workgroups per segment and part
     const int32_t* seg = plist + (size_t)shard * pcap;
-    const int hb = (b >> 3) / NSHARD;
+    const int hb = ((b >> 3) / CS) / NSHARD;
     int tile = ((hb >> 2) << 5) + ((b & 7) << 2) + (hb & 3);
     const int n = pcount[shard * CSTRIDE];
     int e = tile * 16 + cl;
@@ -132,7 +145,7 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(const 
     if (a.cum_dst && b == 0)
         for (int i = (int)threadIdx.x; i < a.n_cum; i += (int)blockDim.x) a.cum_dst[i] += a.cum_src[i];
 
-    const bool do_prop = a.has_next && wave == 0;
+    const bool do_prop = a.has_next && wave == 0 && part == 0;
     while (tile * 16 < n) {
         const bool vrow = e < n;
         const int q = vrow ? qspec : 0;
@@ -155,7 +168,7 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(const 
         f4v zo[NCB];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb)
-            zo[cb] = *reinterpret_cast<const f4v*>(zrow + min((cw * NCB + cb) * 16 + 4 * g, COUT - 4));
+            zo[cb] = *reinterpret_cast<const f4v*>(zrow + min((part * NCBW + cw * NCB + cb) * 16 + 4 * g, COUT - 4));
         // sparse backbones: only a site active now or before can change, and
         // only such sites go to the next layer's list
         bool now = true, prev = true;
@@ -177,7 +190,7 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(const 
         }
 
         const char* dbase = static_cast<const char*>(a.delta_in) + g * 16;
-        const uint4* wbase = static_cast<const uint4*>(a.wpack) + (size_t)cw * NCB * 64 + lane;
+        const uint4* wbase = static_cast<const uint4*>(a.wpack) + (size_t)(part * NCBW + cw * NCB) * 64 + lane;
         f4v acc[NCB];
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb) acc[cb] = f4v{0.f, 0.f, 0.f, 0.f};
@@ -279,12 +292,12 @@ __global__ __launch_bounds__(64 * LayerShape<COUT>::NW) void layer_kernel(const 
         if (vrow && ks == 0) {
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) {
-                const int co0 = (cw * NCB + cb) * 16 + 4 * g;
+                const int co0 = (part * NCBW + cw * NCB + cb) * 16 + 4 * g;
                 if (COUT % 16 == 0 || co0 < COUT) epilogue4<COUT, BF16>(a, q, co0, zo[cb], acc[cb], now, prev);
             }
         }
         if constexpr (SPARSE) {
-            if (a.mnext.memb && wave == 0 && g == 0 && vrow && now != prev)
+            if (a.mnext.memb && wave == 0 && part == 0 && g == 0 && vrow && now != prev)
                 memb_spread(a.mnext, q, a.Hout, a.Wout, now ? 1 : -1, a.epoch);
         }
         if (do_prop) prop_finish<4>(a.next, a.epoch, shard, pb);
@@ -472,9 +485,10 @@ static hipError_t launch_shape(const LayerArgs& a, int grid, const LaunchCtx& c)
         return launch_kernel(c, layer_kernel_wide<CI, CO, S, BF16, SPARSE>, dim3(gl * NH * NSHARD), dim3(256), a.list,
                              a.count, a.cap, a);
     } else {
-        // whole runs of 4 tiles on every XCD for every segment
-        grid = std::max(32 * NSHARD, grid / (32 * NSHARD) * (32 * NSHARD));
-        return launch_kernel(c, layer_kernel<CI, CO, S, BF16, SPARSE>, dim3(grid), dim3(64 * LayerShape<CO>::NW), a.list,
+        // whole runs of 4 tiles on every XCD for every segment and cout part
+        constexpr int GU = 32 * NSHARD * LayerShape<CO, S>::CS;
+        grid = std::max(GU, grid / GU * GU);
+        return launch_kernel(c, layer_kernel<CI, CO, S, BF16, SPARSE>, dim3(grid), dim3(64 * LayerShape<CO, S>::NW), a.list,
                              a.count, a.cap, a);
     }
 }
