@@ -325,29 +325,41 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(c
 // block 1; lane l of a 16-byte-per-lane copy lands at base + 16*l, which is
 // the MFMA operand layout.  Taps without a changed input in either tile are
 // skipped by the whole workgroup.
+#ifndef SSC_WIDE_KH
+#define SSC_WIDE_KH 2
+#endif
 template <int CIN, int COUT, bool BF16>
 struct WideShape {
     static constexpr int KTOT = BF16 ? 2 * CIN : CIN;
     static constexpr int NCH = KTOT / (BF16 ? 32 : 16);    // 1 KB operand chunks per tap
     static constexpr int NCBT = COUT / 16;
     static constexpr int NH = NCBT / 2;                     // workgroups per tile pair
+    static constexpr int KH = NCH <= 8 ? SSC_WIDE_KH : 1;  // groups of 4 wavefronts over the taps
 };
 
 // plist, pcount, pcap: as for layer_kernel (preloaded copies of a.list,
 // a.count, a.cap).
+// With KH > 1 the workgroup holds KH groups of the four wavefronts: group k
+// contracts the k-th, (k+KH)-th, ... of the tile pair's active taps through
+// a stage of its own, so KH taps' copies and matrix work are in flight at
+// once, and groups 1..KH-1 add their partial sums into group 0 through LDS,
+// in group order.  Every group runs the same number of tap steps (the last
+// one idle where the taps do not divide evenly), so the barriers match.
 template <int CIN, int COUT, int S, bool BF16, bool SPARSE>
-__global__ __launch_bounds__(256) void layer_kernel_wide(const int32_t* __restrict__ plist,
-                                                          const int32_t* __restrict__ pcount, int pcap, LayerArgs a) {
+__global__ __launch_bounds__((256 * WideShape<CIN, COUT, BF16>::KH)) void layer_kernel_wide(
+    const int32_t* __restrict__ plist, const int32_t* __restrict__ pcount, int pcap, LayerArgs a) {
     using W = WideShape<CIN, COUT, BF16>;
-    constexpr int NCH = W::NCH, NCBT = W::NCBT, NH = W::NH;
+    constexpr int NCH = W::NCH, NCBT = W::NCBT, NH = W::NH, KH = W::KH;
     constexpr int ROWB_IN = 4 * CIN;
     static_assert(NCH % 2 == 0 && NCBT % 2 == 0, "shape");
-    __shared__ uint4 stage[4][NCH][64];
+    __shared__ uint4 stage[KH][4][NCH][64];
+    __shared__ f4v red[KH > 1 ? KH - 1 : 1][4][64];
     __shared__ int tapmask;
 
-    const int lane = (int)(threadIdx.x & 63u), wave = (int)(threadIdx.x >> 6);
+    const int lane = (int)(threadIdx.x & 63u), wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int cl = lane & 15, g = lane >> 4;
-    const int tp = wave & 1, cbl = wave >> 1;          // tile and cout block of this wavefront
+    const int kh = wave >> 2, w4 = wave & 3;           // tap group; role in the group
+    const int tp = w4 & 1, cbl = w4 >> 1;              // tile and cout block of this wavefront
     const int b = (int)blockIdx.x;
     const int h = b % NH;                              // cout blocks 2h, 2h+1
     const int shard = (b / NH) % NSHARD;
@@ -355,7 +367,8 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(const int32_t* __restri
     const int32_t* seg = plist + (size_t)shard * pcap;
     const int n = pcount[shard * CSTRIDE];
     const int cbg = 2 * h + cbl;                       // global cout block of this wavefront
-    const bool do_prop = a.has_next && h == 0 && cbl == 0;
+    const bool lead = kh == 0;                         // the group that finishes the tile
+    const bool do_prop = a.has_next && h == 0 && cbl == 0 && lead;
     const char* dbase = static_cast<const char*>(a.delta_in) + g * 16;
     const uint4* wbase = static_cast<const uint4*>(a.wpack) + lane;
 
@@ -389,28 +402,41 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(const int32_t* __restri
         __syncthreads();
         if (lane == 0 && mask) atomicOr(&tapmask, (int)mask);
         __syncthreads();
-        unsigned taps = (unsigned)tapmask;
+        const unsigned taps = (unsigned)__builtin_amdgcn_readfirstlane(tapmask);
+        // this group's taps: every KH-th active one from the kh-th on
+        unsigned mine = 0u;
+        {
+            int k = 0;
+#pragma unroll
+            for (int t = 0; t < 9; ++t)
+                if ((taps >> t) & 1u) {
+                    if (k % KH == kh) mine |= 1u << t;
+                    ++k;
+                }
+        }
+        const int nsteps = (__builtin_popcount(taps) + KH - 1) / KH;
 
-        // copies of tap t into the stage: the two wavefronts of a tile share
-        // its delta chunks, the two wavefronts of a cout block its weights
+        // copies of tap t into the group's stage: the two wavefronts of a
+        // tile share its delta chunks, the two wavefronts of a cout block its
+        // weights
         auto issue = [&](int t) __attribute__((always_inline)) {
             const int row = max(rows[t], 0);
 #pragma unroll
             for (int c = cbl; c < NCH; c += 2)
                 __builtin_amdgcn_global_load_lds(
                     (const __attribute__((address_space(1))) void*)(dbase + (size_t)row * ROWB_IN + c * 64),
-                    (__attribute__((address_space(3))) void*)&stage[tp][c][0], 16, 0, 0);
+                    (__attribute__((address_space(3))) void*)&stage[kh][tp][c][0], 16, 0, 0);
 #pragma unroll
             for (int c = tp; c < NCH; c += 2)
                 __builtin_amdgcn_global_load_lds(
                     (const __attribute__((address_space(1))) void*)(wbase + ((size_t)(t * NCH + c) * NCBT + cbg) * 64),
-                    (__attribute__((address_space(3))) void*)&stage[2 + cbl][c][0], 16, 0, 0);
+                    (__attribute__((address_space(3))) void*)&stage[kh][2 + cbl][c][0], 16, 0, 0);
         };
 
-        // one stage buffer: a tap's operands move to registers, then the
-        // copies of the next tap overwrite the stage while the matrix cores
-        // work; a small stage lets two workgroups share a compute unit, so
-        // one computes while the other waits for its copies
+        // one stage buffer per group: a tap's operands move to registers,
+        // then the copies of the group's next tap overwrite the stage while
+        // the matrix cores work; a small stage lets two workgroups share a
+        // compute unit, so one computes while the other waits for its copies
         // take the next layer's list positions now: the counter's round trip
         // then overlaps the taps instead of ending the tile (measured on c3:
         // 364 -> 355 us per stride; in the narrow kernel the same move stalls
@@ -418,38 +444,55 @@ __global__ __launch_bounds__(256) void layer_kernel_wide(const int32_t* __restri
         PropSlots<4> ps;
         if (do_prop) prop_reserve<4>(a.next, a.epoch, shard, pb, ps);
         f4v acc[1] = {f4v{0.f, 0.f, 0.f, 0.f}};
-        if (taps) issue(__builtin_ctz(taps));
-        while (taps) {
-            const int t = __builtin_ctz(taps);
-            taps &= taps - 1u;
+        if (mine) issue(__builtin_ctz(mine));
+        for (int step = 0; step < nsteps; ++step) {
+            const bool have = mine != 0u;
+            const int t = have ? __builtin_ctz(mine) : 0;
+            mine &= mine - 1u;
             __builtin_amdgcn_s_waitcnt(0);             // this wavefront's copies of tap t
             __syncthreads();                           // everyone's copies of tap t
             uint4 av[NCH], bv[NCH];
-            const uint32_t m = rows[t] >= 0 ? ~0u : 0u;   // unchanged input: zero row
+            const uint32_t m = have && rows[t] >= 0 ? ~0u : 0u;   // unchanged input: zero row
 #pragma unroll
             for (int c = 0; c < NCH; ++c) {
-                const uint4 x = stage[tp][c][lane];
+                const uint4 x = stage[kh][tp][c][lane];
                 av[c] = make_uint4(x.x & m, x.y & m, x.z & m, x.w & m);
-                bv[c] = stage[2 + cbl][c][lane];
+                bv[c] = stage[kh][2 + cbl][c][lane];
             }
-            if (taps) {
+            if (step + 1 < nsteps) {
                 __builtin_amdgcn_s_waitcnt(0);         // this wavefront's stage reads are done
-                __syncthreads();                       // everyone's: the stage is free
-                issue(__builtin_ctz(taps));
+                __syncthreads();                       // everyone's: the stages are free
+                if (mine) issue(__builtin_ctz(mine));
             }
+            if (have) {
 #pragma unroll
-            for (int c = 0; c < NCH; ++c) {
-                const uint4 bb[1] = {bv[c]};
-                mfma_chunk<BF16, 1>(acc, av[c], bb);
+                for (int c = 0; c < NCH; ++c) {
+                    const uint4 bb[1] = {bv[c]};
+                    mfma_chunk<BF16, 1>(acc, av[c], bb);
+                }
             }
         }
-        if (vrow) epilogue4<COUT, BF16>(a, q, cbg * 16 + 4 * g, zo, acc[0], now, prev);
+        if constexpr (KH > 1) {
+            if (!lead) red[kh - 1][w4][lane] = acc[0];
+            __syncthreads();
+            if (lead) {
+#pragma unroll
+                for (int k = 0; k < KH - 1; ++k) {
+                    const f4v p = red[k][w4][lane];
+                    acc[0].x += p.x;
+                    acc[0].y += p.y;
+                    acc[0].z += p.z;
+                    acc[0].w += p.w;
+                }
+            }
+        }
+        if (vrow && lead) epilogue4<COUT, BF16>(a, q, cbg * 16 + 4 * g, zo, acc[0], now, prev);
         if constexpr (SPARSE) {
-            if (a.mnext.memb && h == 0 && cbl == 0 && g == 0 && vrow && now != prev)
+            if (a.mnext.memb && h == 0 && cbl == 0 && g == 0 && lead && vrow && now != prev)
                 memb_spread(a.mnext, q, a.Hout, a.Wout, now ? 1 : -1, a.epoch);
         }
         if (do_prop) prop_write<4>(a.next, shard, pb, ps);
-        __syncthreads();                               // the stage buffers are free again
+        __syncthreads();                               // the stages and partial sums are free again
     }
     if (a.cum_dst && b == 0)
         for (int i = (int)threadIdx.x; i < a.n_cum; i += (int)blockDim.x) a.cum_dst[i] += a.cum_src[i];
@@ -482,8 +525,9 @@ static hipError_t launch_shape(const LayerArgs& a, int grid, const LaunchCtx& c)
         constexpr int NH = WideShape<CI, CO, BF16>::NH;
         int gl = std::max(1, grid / (2 * NH * NSHARD));
         gl = std::min(gl, std::max(1, (a.cap + 31) / 32));
-        return launch_kernel(c, layer_kernel_wide<CI, CO, S, BF16, SPARSE>, dim3(gl * NH * NSHARD), dim3(256), a.list,
-                             a.count, a.cap, a);
+        constexpr int KH = WideShape<CI, CO, BF16>::KH;
+        return launch_kernel(c, layer_kernel_wide<CI, CO, S, BF16, SPARSE>, dim3(gl * NH * NSHARD), dim3(256 * KH),
+                             a.list, a.count, a.cap, a);
     } else {
         // whole runs of 4 tiles on every XCD for every segment and cout part
         constexpr int GU = 32 * NSHARD * LayerShape<CO, S>::CS;

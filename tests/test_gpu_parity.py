@@ -44,6 +44,15 @@ def test_c4_backbone_bf16_200_strides():
     run_stream("c4", map_every=50)
 
 
+@pytest.mark.parametrize("name,n", [("c3", 20), ("c4", 30)])
+def test_one_launch_wide_layers(name, n, monkeypatch):
+    """The wide stride-1 layers in the one-launch output-stationary kernel
+    (SSCATER_FUSED_WIDE=1, read when a handle is created) instead of the
+    contraction and tap sum: its tap groups over the nine stride-1 taps."""
+    monkeypatch.setenv("SSCATER_FUSED_WIDE", "1")
+    run_stream(name, n_strides=n, map_every=10)
+
+
 def test_c5_four_concurrent_streams():
     name = "c5"
     wl = S.workload(name)
