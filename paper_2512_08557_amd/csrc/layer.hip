@@ -65,6 +65,24 @@ namespace ssc {
 // 64->128: ~80 tiles, fewer than the compute units), so a wavefront's matrix
 // work is the chain that ends the launch.  (Stride 1 with ~170 tiles: the
 // split only doubles the gathers; measured 1 us slower per launch.)
+// bf16 weights: the pair form contracts [Y_new | Y_old] against [W | -W];
+// the packed weights hold W once (chunk c of the pair uses weight chunk
+// c % N) and the kernels flip the sign bits of the delta's old half
+// instead, which gives bit-identical products ((-y) * w == y * (-w)).  With
+// cin = 16 the one 32-value chunk holds [W | W].
+template <int CIN, bool BF16>
+struct WeightChunks {
+    static constexpr int N = BF16 ? (CIN >= 32 ? CIN / 32 : 1) : CIN / 16;
+};
+
+// The 8 bf16 pair values of lane group g in chunk c, their sign bits flipped
+// where they belong to the old half (pair position >= CIN).
+template <int CIN>
+__device__ __forceinline__ uint4 old_half_negated(uint4 v, int c, int g) {
+    const uint32_t s = c * 32 + 8 * g >= CIN ? 0x80008000u : 0u;
+    return make_uint4(v.x ^ s, v.y ^ s, v.z ^ s, v.w ^ s);
+}
+
 template <int COUT, int S = 1>
 struct LayerShape {
     static constexpr int NCBT = (COUT + 15) / 16;           // 16-wide cout blocks
@@ -111,6 +129,7 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(c
     constexpr int KTOT = BF16 ? 2 * CIN : CIN;   // contraction length per tap
     constexpr int KCH = BF16 ? 32 : 16;          // k per 64-byte chunk
     constexpr int NCH = KTOT / KCH;
+    constexpr int NCHW = WeightChunks<CIN, BF16>::N;   // weight chunks per tap
     constexpr int ROWB_IN = 4 * CIN;             // input delta row bytes (fp32, or bf16 pair)
     constexpr int ROWB_OUT = 4 * COUT;
 
@@ -251,7 +270,7 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(c
             const int st = KS == 1 ? i : min(ks + KS * i, NSTEP - 1);
             const int c = st % NCH;
             abuf[i] = *reinterpret_cast<const uint4*>(dbase + (size_t)max(srow[i], 0) * ROWB_IN + c * 64);
-            const uint4* wp = wbase + (size_t)st * NCBT * 64;
+            const uint4* wp = wbase + (size_t)((st / NCH) * NCHW + c % NCHW) * NCBT * 64;
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) bbuf[i][cb] = wp[cb * 64];
         };
@@ -262,6 +281,10 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(c
             if (i + PF < NSW) issue(i + PF);
             uint4 av = abuf[i];
             if (srow[i] < 0) av = make_uint4(0u, 0u, 0u, 0u);
+            if constexpr (BF16) {
+                const int st = KS == 1 ? i : min(ks + KS * i, NSTEP - 1);
+                av = old_half_negated<CIN>(av, st % NCH, g);
+            }
             if (sany[i]) mfma_chunk(av, bbuf[i]);
             // keep the scheduler from hoisting later loads past this step
             __builtin_amdgcn_sched_barrier(0);
@@ -332,6 +355,7 @@ template <int CIN, int COUT, bool BF16>
 struct WideShape {
     static constexpr int KTOT = BF16 ? 2 * CIN : CIN;
     static constexpr int NCH = KTOT / (BF16 ? 32 : 16);    // 1 KB operand chunks per tap
+    static constexpr int NCHW = WeightChunks<CIN, BF16>::N; // weight chunks per tap
     static constexpr int NCBT = COUT / 16;
     static constexpr int NH = NCBT / 2;                     // workgroups per tile pair
     static constexpr int KH = NCH <= 8 ? SSC_WIDE_KH : 1;  // groups of 4 wavefronts over the taps
@@ -349,9 +373,9 @@ template <int CIN, int COUT, int S, bool BF16, bool SPARSE>
 __global__ __launch_bounds__((256 * WideShape<CIN, COUT, BF16>::KH)) void layer_kernel_wide(
     const int32_t* __restrict__ plist, const int32_t* __restrict__ pcount, int pcap, LayerArgs a) {
     using W = WideShape<CIN, COUT, BF16>;
-    constexpr int NCH = W::NCH, NCBT = W::NCBT, NH = W::NH, KH = W::KH;
+    constexpr int NCH = W::NCH, NCHW = W::NCHW, NCBT = W::NCBT, NH = W::NH, KH = W::KH;
     constexpr int ROWB_IN = 4 * CIN;
-    static_assert(NCH % 2 == 0 && NCBT % 2 == 0, "shape");
+    static_assert(NCH % 2 == 0 && NCHW % 2 == 0 && NCBT % 2 == 0, "shape");
     __shared__ uint4 stage[KH][4][NCH][64];
     __shared__ f4v red[KH > 1 ? KH - 1 : 1][4][64];
     __shared__ int tapmask;
@@ -427,9 +451,9 @@ __global__ __launch_bounds__((256 * WideShape<CIN, COUT, BF16>::KH)) void layer_
                     (const __attribute__((address_space(1))) void*)(dbase + (size_t)row * ROWB_IN + c * 64),
                     (__attribute__((address_space(3))) void*)&stage[kh][tp][c][0], 16, 0, 0);
 #pragma unroll
-            for (int c = tp; c < NCH; c += 2)
+            for (int c = tp; c < NCHW; c += 2)
                 __builtin_amdgcn_global_load_lds(
-                    (const __attribute__((address_space(1))) void*)(wbase + ((size_t)(t * NCH + c) * NCBT + cbg) * 64),
+                    (const __attribute__((address_space(1))) void*)(wbase + ((size_t)(t * NCHW + c) * NCBT + cbg) * 64),
                     (__attribute__((address_space(3))) void*)&stage[kh][2 + cbl][c][0], 16, 0, 0);
         };
 
@@ -451,14 +475,16 @@ __global__ __launch_bounds__((256 * WideShape<CIN, COUT, BF16>::KH)) void layer_
             mine &= mine - 1u;
             __builtin_amdgcn_s_waitcnt(0);             // this wavefront's copies of tap t
             __syncthreads();                           // everyone's copies of tap t
-            uint4 av[NCH], bv[NCH];
+            uint4 av[NCH], bv[NCHW];
             const uint32_t m = have && rows[t] >= 0 ? ~0u : 0u;   // unchanged input: zero row
 #pragma unroll
             for (int c = 0; c < NCH; ++c) {
                 const uint4 x = stage[kh][tp][c][lane];
                 av[c] = make_uint4(x.x & m, x.y & m, x.z & m, x.w & m);
-                bv[c] = stage[kh][2 + cbl][c][lane];
+                if constexpr (BF16) av[c] = old_half_negated<CIN>(av[c], c, g);
             }
+#pragma unroll
+            for (int c = 0; c < NCHW; ++c) bv[c] = stage[kh][2 + cbl][c][lane];
             if (step + 1 < nsteps) {
                 __builtin_amdgcn_s_waitcnt(0);         // this wavefront's stage reads are done
                 __syncthreads();                       // everyone's: the stages are free
@@ -467,7 +493,7 @@ __global__ __launch_bounds__((256 * WideShape<CIN, COUT, BF16>::KH)) void layer_
             if (have) {
 #pragma unroll
                 for (int c = 0; c < NCH; ++c) {
-                    const uint4 bb[1] = {bv[c]};
+                    const uint4 bb[1] = {bv[c % NCHW]};
                     mfma_chunk<BF16, 1>(acc, av[c], bb);
                 }
             }
@@ -556,14 +582,15 @@ hipError_t launch_layer(const LayerArgs& a, int cin, int cout, int stride, bool 
 // weight repacking (host)
 // ---------------------------------------------------------------------------
 size_t wpack_elems(int cin, int cout, bool bf16) {
-    return (size_t)9 * (size_t)(bf16 ? 2 * cin : cin) * (size_t)((cout + 15) / 16 * 16);
+    return (size_t)9 * (size_t)(bf16 ? std::max(cin, 32) : cin) * (size_t)((cout + 15) / 16 * 16);
 }
 
 // Layout, in 16-byte lane vectors: [tap t][chunk c][cout block cb][lane l],
 // lane l of block cb holds output channel cb*16 + l%16 and the k-group l/16 of
-// chunk c: fp32 k = c*16 + 4*(l/16) + e (e < 4); bf16 k = c*32 + 8*(l/16) + e
-// (e < 8) over the pair [W | -W].  Output channels past cout (cout = 8) are
-// zero.
+// chunk c: fp32 k = c*16 + 4*(l/16) + e (e < 4), cin/16 chunks; bf16 k =
+// c*32 + 8*(l/16) + e (e < 8), input channel k % cin, max(cin/32, 1) chunks
+// (the kernels apply them to both halves of the pair).  Output channels past
+// cout (cout = 8) are zero.
 void pack_weights(const void* w_oihw, int cin, int cout, bool bf16, void* dst) {
     const int ncbt = (cout + 15) / 16;
     if (!bf16) {
@@ -583,18 +610,16 @@ void pack_weights(const void* w_oihw, int cin, int cout, bool bf16, void* dst) {
     } else {
         const uint16_t* w = static_cast<const uint16_t*>(w_oihw);
         uint16_t* out = static_cast<uint16_t*>(dst);
-        const int nch = (2 * cin) / 32;
+        const int nch = std::max(cin / 32, 1);
         for (int t = 0; t < 9; ++t)
             for (int c = 0; c < nch; ++c)
                 for (int cb = 0; cb < ncbt; ++cb)
                     for (int l = 0; l < 64; ++l)
                         for (int e = 0; e < 8; ++e) {
                             const int co = cb * 16 + l % 16;
-                            const int k = c * 32 + 8 * (l / 16) + e;
-                            const int ci = k < cin ? k : k - cin;
-                            uint16_t v = co < cout ? w[(((size_t)co * cin + ci) * 3 + t / 3) * 3 + t % 3] : 0;
-                            if (k >= cin) v ^= 0x8000u;   // -W: exact sign flip (-0 for the padding)
-                            out[((((size_t)t * nch + c) * ncbt + cb) * 64 + l) * 8 + e] = v;
+                            const int ci = (c * 32 + 8 * (l / 16) + e) % cin;
+                            out[((((size_t)t * nch + c) * ncbt + cb) * 64 + l) * 8 + e] =
+                                co < cout ? w[(((size_t)co * cin + ci) * 3 + t / 3) * 3 + t % 3] : 0;
                         }
     }
 }
