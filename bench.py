@@ -340,7 +340,7 @@ def short_kernel(name: str) -> str:
         return f"detect_sorted_kernel<{t[0]},{dt(t[1])}>"
     if fn == "detect_kernel" and len(t) in (3, 4):
         return f"detect_kernel<{t[0]},{dt(t[1])},{'vanished' if t[2] == 'true' else 'present'}>"
-    if fn in ("layer_kernel", "layer_kernel_wide") and len(t) in (4, 5):
+    if fn in ("layer_kernel", "layer_kernel_wide") and len(t) in (4, 5, 6):
         return f"{fn}<{t[0]},{t[1]},{t[2]},{dt(t[3])}>"
     if fn == "contract_kernel" and len(t) == 3:
         return f"contract_kernel<{t[0]},{t[1]},{dt(t[2])}>"

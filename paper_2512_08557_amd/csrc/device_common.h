@@ -105,51 +105,83 @@ __device__ __forceinline__ bool memb_prev(uint64_t w, uint32_t epoch) {
 }
 
 // Counts of the next regular layer: +-1 at every output site whose receptive
-// field holds `cell` (the same stride rule as the change lists).  The targets'
-// words are loaded together and their compare-and-swaps issued together;
-// only a target that another lane changed in between goes round again.
-__device__ __forceinline__ void memb_spread(const MembTarget& t, int cell, int hin, int win, int delta,
-                                            uint32_t epoch) {
-    const unsigned long long ep = epoch & 0x7FFFFFFFu;
+// field holds `cell` (the same stride rule as the change lists), in two
+// halves like the propagation: memb_issue computes the targets and loads
+// their words (from clamped, always valid addresses, also where `on` is
+// false, so that no branch joins on the loads), memb_finish compare-and-swaps
+// them.  A swap that lost to another lane or workgroup goes round again; all
+// of a lane's pending targets go round together, so a round costs one round
+// trip however many of them collided.
+struct MembBatch {
+    unsigned long long old[9];   // the targets' words as loaded
+    uint32_t todo;               // bit k: target k exists and is to be updated
+};
+
+// Target k of `cell` (clamped to the grid) and whether it exists.
+__device__ __forceinline__ unsigned long long* memb_target(const MembTarget& t, int cell, int hin, int win, int k,
+                                                            bool& ok) {
     const int img = cell / (hin * win), loc = cell - img * (hin * win);
     const int i = loc / win, j = loc - (loc / win) * win;
-    const size_t obase = (size_t)img * t.Hout * t.Wout;
-    unsigned long long* ptr[9];
-    unsigned long long old[9];
-    bool todo[9];
+    int rn = i - k / 3 + 1, cn = j - k % 3 + 1;
+    ok = true;
+    if (t.stride == 2) {
+        ok = ((rn | cn) & 1) == 0;
+        rn >>= 1;
+        cn >>= 1;
+    }
+    ok = ok && rn >= 0 && rn < t.Hout && cn >= 0 && cn < t.Wout;
+    return reinterpret_cast<unsigned long long*>(t.memb) + (size_t)img * t.Hout * t.Wout +
+           (size_t)min(max(rn, 0), t.Hout - 1) * t.Wout + min(max(cn, 0), t.Wout - 1);
+}
+
+__device__ __forceinline__ void memb_issue(const MembTarget& t, int cell, int hin, int win, bool on, MembBatch& mb) {
+    mb.todo = 0u;
 #pragma unroll
     for (int k = 0; k < 9; ++k) {
-        int rn = i - k / 3 + 1, cn = j - k % 3 + 1;
-        bool ok = true;
-        if (t.stride == 2) {
-            ok = ((rn | cn) & 1) == 0;
-            rn >>= 1;
-            cn >>= 1;
-        }
-        ok = ok && rn >= 0 && rn < t.Hout && cn >= 0 && cn < t.Wout;
-        todo[k] = ok;
-        ptr[k] = reinterpret_cast<unsigned long long*>(t.memb) + obase +
-                 (size_t)min(max(rn, 0), t.Hout - 1) * t.Wout + min(max(cn, 0), t.Wout - 1);
-        old[k] = ok ? __hip_atomic_load(ptr[k], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0ull;
+        bool ok;
+        unsigned long long* p = memb_target(t, cell, hin, win, k, ok);
+        if (on && ok) mb.todo |= 1u << k;
+        mb.old[k] = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+}
+
+// cell, hin, win: as given to memb_issue.
+__device__ __forceinline__ void memb_finish(const MembTarget& t, int cell, int hin, int win, MembBatch& mb, int delta,
+                                            uint32_t epoch) {
+    const unsigned long long ep = epoch & 0x7FFFFFFFu;
     auto next_word = [&](unsigned long long w) {
         const uint32_t cnt = (uint32_t)w;
         const unsigned long long was = ((w >> 33) == ep) ? ((w >> 32) & 1ull) : (cnt != 0u ? 1ull : 0ull);
         return (ep << 33) | (was << 32) | (unsigned long long)(uint32_t)(cnt + (uint32_t)delta);
     };
-    unsigned long long got[9];
-#pragma unroll
-    for (int k = 0; k < 9; ++k) got[k] = todo[k] ? atomicCAS(ptr[k], old[k], next_word(old[k])) : 0ull;
+    if (mb.todo == 0u) return;
+    unsigned long long* ptr[9];
 #pragma unroll
     for (int k = 0; k < 9; ++k) {
-        if (!todo[k] || got[k] == old[k]) continue;
-        unsigned long long o = got[k];
-        for (;;) {
-            const unsigned long long g2 = atomicCAS(ptr[k], o, next_word(o));
-            if (g2 == o) break;
-            o = g2;
-        }
+        bool ok;
+        ptr[k] = memb_target(t, cell, hin, win, k, ok);
     }
+    uint32_t todo = mb.todo;
+    while (todo) {
+        unsigned long long got[9];
+#pragma unroll
+        for (int k = 0; k < 9; ++k)
+            got[k] = (todo >> k) & 1u ? atomicCAS(ptr[k], mb.old[k], next_word(mb.old[k])) : 0ull;
+        uint32_t lost = 0u;
+#pragma unroll
+        for (int k = 0; k < 9; ++k) {
+            if (((todo >> k) & 1u) && got[k] != mb.old[k]) lost |= 1u << k;   // retry from the word it found
+            mb.old[k] = got[k];
+        }
+        todo = lost;
+    }
+}
+
+__device__ __forceinline__ void memb_spread(const MembTarget& t, int cell, int hin, int win, int delta,
+                                            uint32_t epoch) {
+    MembBatch mb;
+    memb_issue(t, cell, hin, win, true, mb);
+    memb_finish(t, cell, hin, win, mb, delta, epoch);
 }
 
 // prop_finish in two halves, so that the counter's round trip overlaps other

@@ -117,7 +117,9 @@ __device__ __forceinline__ void mfma_chunk(f4v (&acc)[NCB], const uint4 av, cons
 // plist, pcount, pcap are a.list, a.count, a.cap passed again as leading
 // scalar arguments: the build preloads them into SGPRs, so the list entry and
 // count loads that open every tile need not wait for the argument fetch.
-template <int CIN, int COUT, int S, bool BF16, bool SPARSE>
+// SPREAD (with SPARSE): the layer is regular and the next regular layer's
+// active-set counts follow its sites (a.mnext set).
+template <int CIN, int COUT, int S, bool BF16, bool SPARSE, bool SPREAD>
 __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(const int32_t* __restrict__ plist,
                                                                           const int32_t* __restrict__ pcount, int pcap,
                                                                           LayerArgs a) {
@@ -207,6 +209,12 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(c
             rows[t] = (inb[t] && ev[t] == a.epoch) ? cell[t] : -1;
             any[t] = __ballot(rows[t] >= 0) != 0ull;    // no changed input under this tap: skip it
         }
+        // sparse, a regular layer followed by another one (SPREAD): the next
+        // regular layer's words of the sites whose activity flips, loaded now
+        // so that only their swaps end the tile
+        MembBatch mbt;
+        const bool spread = SPREAD && wave == 0 && part == 0;
+        if (spread) memb_issue(a.mnext, q, a.Hout, a.Wout, g == 0 && vrow && now != prev, mbt);
 
         const char* dbase = static_cast<const char*>(a.delta_in) + g * 16;
         const uint4* wbase = static_cast<const uint4*>(a.wpack) + (size_t)(part * NCBW + cw * NCB) * 64 + lane;
@@ -319,10 +327,7 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(c
                 if (COUT % 16 == 0 || co0 < COUT) epilogue4<COUT, BF16>(a, q, co0, zo[cb], acc[cb], now, prev);
             }
         }
-        if constexpr (SPARSE) {
-            if (a.mnext.memb && wave == 0 && part == 0 && g == 0 && vrow && now != prev)
-                memb_spread(a.mnext, q, a.Hout, a.Wout, now ? 1 : -1, a.epoch);
-        }
+        if (spread) memb_finish(a.mnext, q, a.Hout, a.Wout, mbt, now ? 1 : -1, a.epoch);
         if (do_prop) prop_finish<4>(a.next, a.epoch, shard, pb);
 
         tile += GS;
@@ -558,8 +563,12 @@ static hipError_t launch_shape(const LayerArgs& a, int grid, const LaunchCtx& c)
         // whole runs of 4 tiles on every XCD for every segment and cout part
         constexpr int GU = 32 * NSHARD * LayerShape<CO, S>::CS;
         grid = std::max(GU, grid / GU * GU);
-        return launch_kernel(c, layer_kernel<CI, CO, S, BF16, SPARSE>, dim3(grid), dim3(64 * LayerShape<CO, S>::NW), a.list,
-                             a.count, a.cap, a);
+        if constexpr (SPARSE)
+            if (a.mnext.memb)
+                return launch_kernel(c, layer_kernel<CI, CO, S, BF16, true, true>, dim3(grid),
+                                     dim3(64 * LayerShape<CO, S>::NW), a.list, a.count, a.cap, a);
+        return launch_kernel(c, layer_kernel<CI, CO, S, BF16, SPARSE, false>, dim3(grid), dim3(64 * LayerShape<CO, S>::NW),
+                             a.list, a.count, a.cap, a);
     }
 }
 

@@ -98,3 +98,7 @@ def test_detection_slot_names_follow_the_detection_form(monkeypatch):
     assert bench.short_kernel("void ssc::detect_kernel<128, true, true, false>(ssc::DetectArgs)") == \
         "detect_kernel<128,bf16,vanished>"
     assert bench.launches_per_stride("detect_sorted_kernel<256,f32>", wl) == 1
+    assert bench.short_kernel("void ssc::layer_kernel<64, 64, 2, false, true, true>(int const*, int const*, int, "
+                              "ssc::LayerArgs)") == "layer_kernel<64,64,2,f32>"
+    assert bench.short_kernel("void ssc::layer_kernel_wide<128, 256, 2, true, false>(int const*, int const*, int, "
+                              "ssc::LayerArgs)") == "layer_kernel_wide<128,256,2,bf16>"
