@@ -16,7 +16,7 @@
 // in one launch (each workgroup merges its stretch of the two lists).
 // Sparse backbones (SPARSE): the pillar set is itself an input, so a pillar
 // that appeared or vanished is changed whatever its values, and it moves the
-// first layer's active-set counts (memb_spread).
+// first layer's active-set counts (memb_issue, memb_swap, memb_settle).
 //
 // Layout: G = row_bytes / 16 lanes share one feature row, each lane moving 16
 // bytes, so a 64-channel fp32 row (256 B) is one fully coalesced 16-lane
@@ -47,9 +47,15 @@ __device__ __forceinline__ void emit_rows(const DetectArgs& a, int p, int pc, bo
     const unsigned long long bal = __ballot(d);
     const unsigned long long gm = (G == 64 ? ~0ull : ((1ull << G) - 1ull)) << gbase;
     const bool gd = (bal & gm) != 0ull;
-    // stamp the first layer's footprint while the rows are written
+    // stamp the first layer's footprint while the rows are written; a
+    // toggled pillar's active-set targets load in the same round trip
     PropBatch<G> pb;
     prop_issue<G, false>(a.next, pc, gd, sub, a.epoch, pb);
+    MembBatch mb;
+    const int md = vanish ? -1 : 1;
+    // (only a wavefront with a toggle loads them: the branch is uniform)
+    const bool mtog = SPARSE && __ballot(tog && sub == 0) != 0ull;
+    if (mtog) memb_issue(a.memb, pc, a.next.Hin, a.next.Win, tog && sub == 0, mb);
     if (gd) {
         char* xrow = static_cast<char*>(a.X) + (size_t)pc * ROWB + sub * 16;
         char* drow = static_cast<char*>(a.delta0) + (size_t)p * DROWB;
@@ -67,11 +73,14 @@ __device__ __forceinline__ void emit_rows(const DetectArgs& a, int p, int pc, bo
         *reinterpret_cast<uint4*>(xrow) = nv;
         if (sub == 0) a.stamp0[p] = a.epoch;
     }
-    if (SPARSE && tog && sub == 0) memb_spread(a.memb, p, a.next.Hin, a.next.Win, vanish ? -1 : 1, a.epoch);
+    // the swaps' round trip overlaps the list append's
+    unsigned long long got[9];
+    if (mtog) memb_swap(a.memb, pc, a.next.Hin, a.next.Win, mb, md, a.epoch, got);
     // |A_0|: one counter per shard, no returned value to wait for
     const int changed = (int)__popcll(__ballot(gd && sub == 0));
     if (lane == 0 && changed) atomicAdd(a.count0 + shard * CSTRIDE, changed);
     prop_finish<G>(a.next, a.epoch, shard, pb);
+    if (mtog) memb_settle(a.memb, pc, a.next.Hin, a.next.Win, mb, md, a.epoch, got);
 }
 
 // Row i of the new list (present pass), valid while i < iend.  a.sorted: the

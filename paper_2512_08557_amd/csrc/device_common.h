@@ -145,36 +145,68 @@ __device__ __forceinline__ void memb_issue(const MembTarget& t, int cell, int hi
     }
 }
 
-// cell, hin, win: as given to memb_issue.
-__device__ __forceinline__ void memb_finish(const MembTarget& t, int cell, int hin, int win, MembBatch& mb, int delta,
-                                            uint32_t epoch) {
+// The word after adding `delta` to the count; the first change of a stride
+// (epoch ep) records whether the site was active before it.
+__device__ __forceinline__ unsigned long long memb_next(unsigned long long w, int delta, unsigned long long ep) {
+    const uint32_t cnt = (uint32_t)w;
+    const unsigned long long was = ((w >> 33) == ep) ? ((w >> 32) & 1ull) : (cnt != 0u ? 1ull : 0ull);
+    return (ep << 33) | (was << 32) | (unsigned long long)(uint32_t)(cnt + (uint32_t)delta);
+}
+
+// memb_finish in two halves, so that the first swaps' round trip can overlap
+// another (memb_swap issues them, memb_settle retries the lost ones); cell,
+// hin, win: as given to memb_issue.
+__device__ __forceinline__ void memb_swap(const MembTarget& t, int cell, int hin, int win, const MembBatch& mb,
+                                          int delta, uint32_t epoch, unsigned long long (&got)[9]) {
     const unsigned long long ep = epoch & 0x7FFFFFFFu;
-    auto next_word = [&](unsigned long long w) {
-        const uint32_t cnt = (uint32_t)w;
-        const unsigned long long was = ((w >> 33) == ep) ? ((w >> 32) & 1ull) : (cnt != 0u ? 1ull : 0ull);
-        return (ep << 33) | (was << 32) | (unsigned long long)(uint32_t)(cnt + (uint32_t)delta);
-    };
+#pragma unroll
+    for (int k = 0; k < 9; ++k) got[k] = mb.old[k];
     if (mb.todo == 0u) return;
+#pragma unroll
+    for (int k = 0; k < 9; ++k) {
+        bool ok;
+        unsigned long long* p = memb_target(t, cell, hin, win, k, ok);
+        if ((mb.todo >> k) & 1u) got[k] = atomicCAS(p, mb.old[k], memb_next(mb.old[k], delta, ep));
+    }
+}
+
+__device__ __forceinline__ void memb_settle(const MembTarget& t, int cell, int hin, int win, MembBatch& mb, int delta,
+                                            uint32_t epoch, const unsigned long long (&got0)[9]) {
+    const unsigned long long ep = epoch & 0x7FFFFFFFu;
+    uint32_t todo = 0u;
+#pragma unroll
+    for (int k = 0; k < 9; ++k) {
+        if (((mb.todo >> k) & 1u) && got0[k] != mb.old[k]) todo |= 1u << k;   // lost: retry from the word it found
+        mb.old[k] = got0[k];
+    }
+    if (todo == 0u) return;
     unsigned long long* ptr[9];
 #pragma unroll
     for (int k = 0; k < 9; ++k) {
         bool ok;
         ptr[k] = memb_target(t, cell, hin, win, k, ok);
     }
-    uint32_t todo = mb.todo;
     while (todo) {
         unsigned long long got[9];
 #pragma unroll
         for (int k = 0; k < 9; ++k)
-            got[k] = (todo >> k) & 1u ? atomicCAS(ptr[k], mb.old[k], next_word(mb.old[k])) : 0ull;
+            got[k] = (todo >> k) & 1u ? atomicCAS(ptr[k], mb.old[k], memb_next(mb.old[k], delta, ep)) : 0ull;
         uint32_t lost = 0u;
 #pragma unroll
         for (int k = 0; k < 9; ++k) {
-            if (((todo >> k) & 1u) && got[k] != mb.old[k]) lost |= 1u << k;   // retry from the word it found
+            if (((todo >> k) & 1u) && got[k] != mb.old[k]) lost |= 1u << k;
             mb.old[k] = got[k];
         }
         todo = lost;
     }
+}
+
+// cell, hin, win: as given to memb_issue.
+__device__ __forceinline__ void memb_finish(const MembTarget& t, int cell, int hin, int win, MembBatch& mb, int delta,
+                                            uint32_t epoch) {
+    unsigned long long got[9];
+    memb_swap(t, cell, hin, win, mb, delta, epoch, got);
+    memb_settle(t, cell, hin, win, mb, delta, epoch, got);
 }
 
 __device__ __forceinline__ void memb_spread(const MembTarget& t, int cell, int hin, int win, int delta,
