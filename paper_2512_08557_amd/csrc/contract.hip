@@ -302,6 +302,10 @@ __global__ __launch_bounds__(256) void tap_sum_kernel(const int32_t* __restrict_
             const float* src = (ch ? a.part + (size_t)cell[t] * N : a.zero) + t * COUT + co0;
             v[t] = __builtin_nontemporal_load(reinterpret_cast<const f4v*>(src));
         }
+        // take the next layer's list positions now: the counter's round trip
+        // then overlaps the contributions' instead of ending the tile
+        PropSlots<16> ps;
+        if (a.has_next && prop_wave) prop_reserve<16>(a.next, a.epoch, shard, pb, ps);
         f4v d = v[0];
 #pragma unroll
         for (int t = 1; t < 9; ++t) {
@@ -315,7 +319,7 @@ __global__ __launch_bounds__(256) void tap_sum_kernel(const int32_t* __restrict_
             if (a.mnext.memb && sub == 0 && vp && nowp != prevp)
                 memb_spread(a.mnext, qp, a.Hout, a.Wout, nowp ? 1 : -1, a.epoch);
         }
-        if (a.has_next && prop_wave) prop_finish<16>(a.next, a.epoch, shard, pb);
+        if (a.has_next && prop_wave) prop_write<16>(a.next, shard, pb, ps);
     }
 }
 
