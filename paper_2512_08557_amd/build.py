@@ -26,6 +26,10 @@ COMMON = [
     # the layer kernels' leading (list, count, cap) arguments arrive in SGPRs,
     # so their first loads need not wait for the kernel-argument fetch
     "-mllvm", "-amdgpu-kernarg-preload-count=5",
+    # every uniform-address atomic here is issued by one lane; the atomic
+    # optimizer would turn it into a wave-wide scan whose readfirstlane waits
+    # for the returned value (and every older load) right after the issue
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-Wall", "-Wno-unused-result", "-I", os.path.join(ROOT, "include"),
 ]
 

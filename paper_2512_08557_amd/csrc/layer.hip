@@ -284,6 +284,12 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(c
         };
 #pragma unroll
         for (int i = 0; i < PF && i < NSW; ++i) issue(i);
+        // the next layer's list positions are taken after the first step:
+        // the footprint atomics went out before the operands, so they have
+        // returned by then, and the counter's round trip overlaps the
+        // following steps instead of ending the tile
+        constexpr int RES = NSW > 1 ? 1 : 0;
+        PropSlots<4> ps;
 #pragma unroll
         for (int i = 0; i < NSW; ++i) {
             if (i + PF < NSW) issue(i + PF);
@@ -294,6 +300,7 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(c
                 av = old_half_negated<CIN>(av, st % NCH, g);
             }
             if (sany[i]) mfma_chunk(av, bbuf[i]);
+            if (i == RES && do_prop) prop_reserve<4>(a.next, a.epoch, shard, pb, ps);
             // keep the scheduler from hoisting later loads past this step
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -328,7 +335,7 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(c
             }
         }
         if (spread) memb_finish(a.mnext, q, a.Hout, a.Wout, mbt, now ? 1 : -1, a.epoch);
-        if (do_prop) prop_finish<4>(a.next, a.epoch, shard, pb);
+        if (do_prop) prop_write<4>(a.next, shard, pb, ps);
 
         tile += GS;
         e = tile * 16 + cl;
@@ -468,8 +475,9 @@ __global__ __launch_bounds__((256 * WideShape<CIN, COUT, BF16>::KH)) void layer_
         // compute unit, so one computes while the other waits for its copies
         // take the next layer's list positions now: the counter's round trip
         // then overlaps the taps instead of ending the tile (measured on c3:
-        // 364 -> 355 us per stride; in the narrow kernel the same move stalls
-        // the first MFMAs on the footprint atomics and is slower)
+        // 364 -> 355 us per stride; the narrow kernel takes them after its
+        // first step, since waiting for the footprint atomics before its
+        // first loads would delay them)
         PropSlots<4> ps;
         if (do_prop) prop_reserve<4>(a.next, a.epoch, shard, pb, ps);
         f4v acc[1] = {f4v{0.f, 0.f, 0.f, 0.f}};
