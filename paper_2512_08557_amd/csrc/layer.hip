@@ -198,10 +198,7 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(c
             now = memb_now(mw);
             prev = memb_prev(mw, a.epoch);
         }
-        // next layer's change list: stamp the footprint in the same round trip
-        // as the stamp and map loads, append the new cells at the end
         PropBatch<4> pb;
-        if (do_prop) prop_issue<4, false>(a.next, q, vrow && (now || prev), g, a.epoch, pb);
         int rows[9];
         bool any[9];
 #pragma unroll
@@ -284,11 +281,15 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(c
         };
 #pragma unroll
         for (int i = 0; i < PF && i < NSW; ++i) issue(i);
-        // the next layer's list positions are taken after the first step:
-        // the footprint atomics went out before the operands, so they have
-        // returned by then, and the counter's round trip overlaps the
-        // following steps instead of ending the tile
-        constexpr int RES = NSW > 1 ? 1 : 0;
+        // next layer's change list: the footprint stamps go out after the
+        // first steps' operand loads (vector-memory results come back in
+        // issue order, so the slower device-scope atomics would otherwise
+        // hold up the first matrix instructions); the list positions are
+        // taken once step PF's operands, issued after the atomics, have
+        // arrived, and the counter's round trip overlaps the remaining steps
+        // instead of ending the tile
+        if (do_prop) prop_issue<4, false>(a.next, q, vrow && (now || prev), g, a.epoch, pb);
+        constexpr int RES = NSW > PF ? PF : NSW - 1;
         PropSlots<4> ps;
 #pragma unroll
         for (int i = 0; i < NSW; ++i) {
