@@ -416,14 +416,23 @@ __global__ __launch_bounds__((256 * WideShape<CIN, COUT, BF16>::KH)) void layer_
         const int qimg = q / (a.Hout * a.Wout), ql = q - qimg * (a.Hout * a.Wout);
         const int qr = ql / a.Wout, qc = ql - (ql / a.Wout) * a.Wout;
         const int ibase = qimg * (a.Hin * a.Win);
+        // the 9 change stamps all in flight together (a ballot between the
+        // loads would wait for each in turn)
+        uint32_t ev[9];
+        int cell[9];
+        bool inb[9];
+#pragma unroll
+        for (int t = 0; t < 9; ++t) {
+            const int ir = S * qr + t / 3 - 1, ic = S * qc + t % 3 - 1;
+            inb[t] = vrow && ir >= 0 && ir < a.Hin && ic >= 0 && ic < a.Win;
+            cell[t] = ibase + min(max(ir, 0), a.Hin - 1) * a.Win + min(max(ic, 0), a.Win - 1);
+            ev[t] = a.stamp_in[cell[t]];
+        }
         int rows[9];
         unsigned mask = 0u;
 #pragma unroll
         for (int t = 0; t < 9; ++t) {
-            const int ir = S * qr + t / 3 - 1, ic = S * qc + t % 3 - 1;
-            const bool inb = vrow && ir >= 0 && ir < a.Hin && ic >= 0 && ic < a.Win;
-            const int cell = ibase + min(max(ir, 0), a.Hin - 1) * a.Win + min(max(ic, 0), a.Win - 1);
-            rows[t] = (inb && a.stamp_in[cell] == a.epoch) ? cell : -1;
+            rows[t] = (inb[t] && ev[t] == a.epoch) ? cell[t] : -1;
             if (__ballot(rows[t] >= 0) != 0ull) mask |= 1u << t;
         }
         const f4v zo = *reinterpret_cast<const f4v*>(a.Z + (size_t)q * COUT + cbg * 16 + 4 * g);
