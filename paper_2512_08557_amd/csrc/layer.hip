@@ -361,9 +361,6 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(c
 // block 1; lane l of a 16-byte-per-lane copy lands at base + 16*l, which is
 // the MFMA operand layout.  Taps without a changed input in either tile are
 // skipped by the whole workgroup.
-#ifndef SSC_WIDE_KH
-#define SSC_WIDE_KH 2
-#endif
 template <int CIN, int COUT, bool BF16>
 struct WideShape {
     static constexpr int KTOT = BF16 ? 2 * CIN : CIN;
@@ -371,7 +368,18 @@ struct WideShape {
     static constexpr int NCHW = WeightChunks<CIN, BF16>::N; // weight chunks per tap
     static constexpr int NCBT = COUT / 16;
     static constexpr int NH = NCBT / 2;                     // workgroups per tile pair
-    static constexpr int KH = NCH <= 8 ? SSC_WIDE_KH : 1;  // groups of 4 wavefronts over the taps
+};
+
+// Groups of four wavefronts over a tile pair's taps: two for a stride-2 layer
+// with at most 8 chunks per tap.  Its output list is ~4x shorter than its
+// input, so its tile pairs leave compute units idle and a workgroup's tap
+// chain ends the launch (c3's 128->256: 192 workgroups).  A stride-1 layer
+// has enough tile pairs to fill the chip, and there the larger workgroup
+// (one per compute unit at these registers) costs a second round (the
+// 504x504 sweep's 128->128: 19.7 -> 24.9 us per launch).
+template <int CIN, int COUT, int S, bool BF16>
+struct WideGroups {
+    static constexpr int KH = S == 2 && WideShape<CIN, COUT, BF16>::NCH <= 8 ? 2 : 1;
 };
 
 // plist, pcount, pcap: as for layer_kernel (preloaded copies of a.list,
@@ -383,10 +391,10 @@ struct WideShape {
 // in group order.  Every group runs the same number of tap steps (the last
 // one idle where the taps do not divide evenly), so the barriers match.
 template <int CIN, int COUT, int S, bool BF16, bool SPARSE>
-__global__ __launch_bounds__((256 * WideShape<CIN, COUT, BF16>::KH)) void layer_kernel_wide(
+__global__ __launch_bounds__((256 * WideGroups<CIN, COUT, S, BF16>::KH)) void layer_kernel_wide(
     const int32_t* __restrict__ plist, const int32_t* __restrict__ pcount, int pcap, LayerArgs a) {
     using W = WideShape<CIN, COUT, BF16>;
-    constexpr int NCH = W::NCH, NCHW = W::NCHW, NCBT = W::NCBT, NH = W::NH, KH = W::KH;
+    constexpr int NCH = W::NCH, NCHW = W::NCHW, NCBT = W::NCBT, NH = W::NH, KH = WideGroups<CIN, COUT, S, BF16>::KH;
     constexpr int ROWB_IN = 4 * CIN;
     static_assert(NCH % 2 == 0 && NCHW % 2 == 0 && NCBT % 2 == 0, "shape");
     __shared__ uint4 stage[KH][4][NCH][64];
@@ -574,7 +582,7 @@ static hipError_t launch_shape(const LayerArgs& a, int grid, const LaunchCtx& c)
         constexpr int NH = WideShape<CI, CO, BF16>::NH;
         int gl = std::max(1, grid / (2 * NH * NSHARD));
         gl = std::min(gl, std::max(1, (a.cap + 31) / 32));
-        constexpr int KH = WideShape<CI, CO, BF16>::KH;
+        constexpr int KH = WideGroups<CI, CO, S, BF16>::KH;
         return launch_kernel(c, layer_kernel_wide<CI, CO, S, BF16, SPARSE>, dim3(gl * NH * NSHARD), dim3(256 * KH),
                              a.list, a.count, a.cap, a);
     } else {
