@@ -12,10 +12,13 @@
 //
 // Per changed input cell the contraction is [cin] x [cin x S*S*cout]: output
 // block ob = (a*S + b)*NCBT + cb holds 16 output channels of one sub-cell.
-// A workgroup takes a tile of 16 input cells and 4*BPW output blocks (4
-// wavefronts, BPW blocks each).  The tile's delta rows (the B operand of every
+// A workgroup takes tiles of 16 input cells for 4*BPW output blocks (4
+// wavefronts, BPW blocks each).  A tile's delta rows (the B operand of every
 // block) are copied once into LDS with asynchronous global->LDS copies shared
-// by the four wavefronts; each wavefront streams the weights of its blocks.
+// by the four wavefronts; each wavefront loads the weights of its blocks once
+// and keeps them in registers for all its tiles (they do not depend on the
+// tile), and the launch holds about two workgroups per compute unit, so that
+// each takes several tiles of a long list.
 #include "device_common.h"
 
 #include <algorithm>
@@ -59,6 +62,14 @@ __global__ __launch_bounds__(256) void upsample_kernel(UpArgs a) {
         obv[k] = o < NOB;
         ob[k] = obv[k] ? o : 0;
     }
+    // this wavefront's weights, for every tile
+    uint4 bw[BPW][NCH];
+    if ((b / OBG) / NSHARD * 16 < n) {
+#pragma unroll
+        for (int k = 0; k < BPW; ++k)
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) bw[k][c] = wbase[((size_t)c * NOB + ob[k]) * 64];
+    }
 
     for (int tile = (b / OBG) / NSHARD; tile * 16 < n; tile += TG) {
         const int e = tile * 16 + cl;
@@ -71,14 +82,11 @@ __global__ __launch_bounds__(256) void upsample_kernel(UpArgs a) {
             __builtin_amdgcn_global_load_lds(
                 (const __attribute__((address_space(1))) void*)(dbase + (size_t)p * ROWB + c * 64),
                 (__attribute__((address_space(3))) void*)&As[c][0], 16, 0, 0);
-        // this wavefront's weights and old Z values, in the same round trip
-        uint4 bw[BPW][NCH];
+        // the old Z values, in the same round trip
         f4v zo[BPW];
         int oc[BPW];
 #pragma unroll
         for (int k = 0; k < BPW; ++k) {
-#pragma unroll
-            for (int c = 0; c < NCH; ++c) bw[k][c] = wbase[((size_t)c * NOB + ob[k]) * 64];
             const int ab = ob[k] / NCBT, cb = ob[k] - (ob[k] / NCBT) * NCBT;
             oc[k] = (S * i + ab / S) * Wn + (S * j + ab % S);
             zo[k] = *reinterpret_cast<const f4v*>(a.Z + (size_t)oc[k] * a.ctot + a.coff + cb * 16 + 4 * g);
@@ -140,8 +148,11 @@ bool upsample_supported(int cin, int cout, int stride) {
 template <int CI, int CO, int S, bool BF16>
 static hipError_t launch_up_shape(const UpArgs& a, int grid, const LaunchCtx& c) {
     using U = UpShape<CI, CO, S, BF16>;
-    // tile slots per (segment, block group); at most ceil(cap / 16) tiles per segment
-    int tg = std::max(1, grid / (U::OBG * NSHARD));
+    // tile slots per (segment, block group), about two workgroups per compute
+    // unit in all (a workgroup keeps its weights over its tiles); at most
+    // ceil(cap / 16) tiles per segment
+    (void)grid;
+    int tg = std::max(1, 512 / (U::OBG * NSHARD));
     tg = std::min(tg, std::max(1, (a.cap + 15) / 16));
     return launch_kernel(c, upsample_kernel<CI, CO, S, BF16>, dim3(tg * U::OBG * NSHARD), dim3(256), a);
 }
