@@ -40,7 +40,8 @@ __global__ __launch_bounds__(256) void upsample_kernel(UpArgs a) {
     using U = UpShape<CIN, COUT, S, BF16>;
     constexpr int NCH = U::NCH, NOB = U::NOB, NCBT = U::NCBT, BPW = U::BPW, OBG = U::OBG;
     constexpr int ROWB = 4 * CIN;                          // delta row bytes (fp32, or bf16 pair)
-    __shared__ uint4 As[NCH][64];
+    __shared__ uint4 As0[NCH][64];
+    __shared__ uint4 As1[NCH][64];
 
     const int lane = (int)(threadIdx.x & 63u), wave = (int)(threadIdx.x >> 6);
     const int cl = lane & 15, g = lane >> 4;
@@ -71,35 +72,65 @@ __global__ __launch_bounds__(256) void upsample_kernel(UpArgs a) {
             for (int c = 0; c < NCH; ++c) bw[k][c] = wbase[((size_t)c * NOB + ob[k]) * 64];
     }
 
-    for (int tile = (b / OBG) / NSHARD; tile * 16 < n; tile += TG) {
-        const int e = tile * 16 + cl;
-        const bool vrow = e < n;
-        const int p = vrow ? seg[min(e, a.cap - 1)] : 0;
+    // tiles tile0, tile0 + TG, ...: the next tile's delta rows (into the other
+    // LDS buffer) and old Z values go out before this tile's matrix work, and
+    // the list entry of the tile after it too, so that only the first tile
+    // waits for its loads.  The two buffers are separate arrays and the loop
+    // takes two tiles per pass, so that the compiler sees a tile's reads and
+    // the next tile's copies touch different arrays (with one array indexed
+    // at run time it waits for every copy before the reads)
+    auto entry = [&](int t) {
+        const int e = t * 16 + cl;
+        return e < n ? seg[min(e, a.cap - 1)] : 0;
+    };
+    auto out_cell = [&](int p, int k) {
         const int i = p / a.Wsrc, j = p - (p / a.Wsrc) * a.Wsrc;
-        // the tile's delta rows: chunk c copied by wavefront c % 4
+        const int ab = ob[k] / NCBT;
+        return (S * i + ab / S) * Wn + (S * j + ab % S);
+    };
+    auto z_at = [&](int oc, int k) {
+        const int cb = ob[k] - (ob[k] / NCBT) * NCBT;
+        return a.Z + (size_t)oc * a.ctot + a.coff + cb * 16 + 4 * g;
+    };
+    int tile = (b / OBG) / NSHARD;
+    int pc = 0, pn = 0;        // cells of this lane's row in this tile and the next
+    f4v zo[BPW];
+    if (tile * 16 < n) {
+        pc = entry(tile);
 #pragma unroll
         for (int c = wave; c < NCH; c += 4)
             __builtin_amdgcn_global_load_lds(
-                (const __attribute__((address_space(1))) void*)(dbase + (size_t)p * ROWB + c * 64),
-                (__attribute__((address_space(3))) void*)&As[c][0], 16, 0, 0);
-        // the old Z values, in the same round trip
-        f4v zo[BPW];
-        int oc[BPW];
+                (const __attribute__((address_space(1))) void*)(dbase + (size_t)pc * ROWB + c * 64),
+                (__attribute__((address_space(3))) void*)&As0[c][0], 16, 0, 0);
 #pragma unroll
-        for (int k = 0; k < BPW; ++k) {
-            const int ab = ob[k] / NCBT, cb = ob[k] - (ob[k] / NCBT) * NCBT;
-            oc[k] = (S * i + ab / S) * Wn + (S * j + ab % S);
-            zo[k] = *reinterpret_cast<const f4v*>(a.Z + (size_t)oc[k] * a.ctot + a.coff + cb * 16 + 4 * g);
-        }
+        for (int k = 0; k < BPW; ++k) zo[k] = *reinterpret_cast<const f4v*>(z_at(out_cell(pc, k), k));
+        pn = entry(tile + TG);
+    }
+    // one tile from `cur`, the next one's rows into `nxt`; false past the end
+    auto step = [&](uint4 (&cur)[NCH][64], uint4 (&nxt)[NCH][64]) __attribute__((always_inline)) {
+        if (tile * 16 >= n) return false;
+        const bool vrow = tile * 16 + cl < n;
         __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();                                   // every chunk of the tile has landed
-
+        __syncthreads();                                   // this tile's chunks have landed; `nxt` is free
+        const bool more = (tile + TG) * 16 < n;
+        f4v zn_next[BPW];
+        int pnn = 0;
+        if (more) {
+#pragma unroll
+            for (int c = wave; c < NCH; c += 4)
+                __builtin_amdgcn_global_load_lds(
+                    (const __attribute__((address_space(1))) void*)(dbase + (size_t)pn * ROWB + c * 64),
+                    (__attribute__((address_space(3))) void*)&nxt[c][0], 16, 0, 0);
+#pragma unroll
+            for (int k = 0; k < BPW; ++k) zn_next[k] = *reinterpret_cast<const f4v*>(z_at(out_cell(pn, k), k));
+            pnn = entry(tile + 2 * TG);
+        }
         f4v acc[BPW];
 #pragma unroll
         for (int k = 0; k < BPW; ++k) acc[k] = f4v{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-            const uint4 av = As[c][lane];
+            const uint4 av = cur[c][lane];
 #pragma unroll
             for (int k = 0; k < BPW; ++k) {
                 if constexpr (BF16) {
@@ -119,17 +150,26 @@ __global__ __launch_bounds__(256) void upsample_kernel(UpArgs a) {
 #pragma unroll
             for (int k = 0; k < BPW; ++k) {
                 if (!obv[k]) continue;
-                const int cb = ob[k] - (ob[k] / NCBT) * NCBT;
                 f4v zn;
                 zn.x = zo[k].x + acc[k].x;
                 zn.y = zo[k].y + acc[k].y;
                 zn.z = zo[k].z + acc[k].z;
                 zn.w = zo[k].w + acc[k].w;
-                *reinterpret_cast<f4v*>(a.Z + (size_t)oc[k] * a.ctot + a.coff + cb * 16 + 4 * g) = zn;
-                if (g == 0) a.stamp[oc[k]] = a.epoch;      // every writer stores the same value
+                const int oc = out_cell(pc, k);
+                *reinterpret_cast<f4v*>(z_at(oc, k)) = zn;
+                if (g == 0) a.stamp[oc] = a.epoch;         // every writer stores the same value
             }
         }
-        __syncthreads();                                   // the chunks are consumed
+        if (more) {
+#pragma unroll
+            for (int k = 0; k < BPW; ++k) zo[k] = zn_next[k];
+        }
+        pc = pn;
+        pn = pnn;
+        tile += TG;
+        return true;
+    };
+    while (step(As0, As1) && step(As1, As0)) {
     }
 }
 
