@@ -130,8 +130,19 @@ __global__ __launch_bounds__(256) void pfn_kernel(PfnArgs a) {
                 k = s + 1;
             }
         const int c = a.list0[(size_t)k * a.cap0 + gi];
+        // the queue bounds, the old canvas value of this lane's channel and
+        // the next layer's footprint stamps in one round trip (none depends
+        // on the new features: the pillar changed because its points did)
         const uint32_t hd = a.head[c];
-        int n = (int)(a.tail[c] - hd);
+        const uint32_t tl = a.tail[c];
+        const int ch = lane < a.C0 ? lane : 0;
+        float xo_f = 0.f;
+        uint16_t xo_b = 0;
+        if constexpr (BF16) xo_b = static_cast<const uint16_t*>(a.X)[(size_t)c * a.C0 + ch];
+        else xo_f = static_cast<const float*>(a.X)[(size_t)c * a.C0 + ch];
+        PropBatch<64> pb;
+        prop_issue<64, false>(a.next, c, true, lane, a.epoch, pb);
+        int n = (int)(tl - hd);
         if (n > a.N) {
             if (lane == 0) flag_error(a.err, ERR_PILLAR_FULL);
             n = a.N;
@@ -141,6 +152,10 @@ __global__ __launch_bounds__(256) void pfn_kernel(PfnArgs a) {
         const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
         const float4 p0 = h0 ? rq[(hd + (uint32_t)lane) % (uint32_t)a.N] : z4;
         const float4 p1 = h1 ? rq[(hd + (uint32_t)lane + 64u) % (uint32_t)a.N] : z4;
+        // the list positions, while the points arrive: the counter's round
+        // trip overlaps them and the feature computation
+        PropSlots<64> ps;
+        prop_reserve<64>(a.next, a.epoch, shard, pb, ps);
         const double sx = wave_sum((double)p0.x + (double)p1.x);
         const double sy = wave_sum((double)p0.y + (double)p1.y);
         const double sz = wave_sum((double)p0.z + (double)p1.z);
@@ -169,20 +184,17 @@ __global__ __launch_bounds__(256) void pfn_kernel(PfnArgs a) {
             if constexpr (BF16) {
                 uint16_t* x = static_cast<uint16_t*>(a.X) + (size_t)c * a.C0 + lane;
                 uint16_t* dr = static_cast<uint16_t*>(a.delta0) + (size_t)c * 2 * a.C0;
-                const uint16_t nb = (uint16_t)f32_to_bf16_bits(f), ob = *x;
+                const uint16_t nb = (uint16_t)f32_to_bf16_bits(f);
                 dr[lane] = nb;                   // the pair [new | old]
-                dr[a.C0 + lane] = ob;
+                dr[a.C0 + lane] = xo_b;
                 *x = nb;
             } else {
                 float* x = static_cast<float*>(a.X) + (size_t)c * a.C0 + lane;
-                const float o = *x;
-                static_cast<float*>(a.delta0)[(size_t)c * a.C0 + lane] = f - o;
+                static_cast<float*>(a.delta0)[(size_t)c * a.C0 + lane] = f - xo_f;
                 *x = f;
             }
         }
-        PropBatch<64> pb;
-        prop_issue<64, false>(a.next, c, true, lane, a.epoch, pb);
-        prop_finish<64>(a.next, a.epoch, shard, pb);
+        prop_write<64>(a.next, shard, pb, ps);
     }
 }
 
