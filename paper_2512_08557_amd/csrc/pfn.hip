@@ -41,6 +41,24 @@ __device__ __forceinline__ void wave_append(int32_t* cnt, int32_t* seg, bool min
     if (mine) seg[base + (int)__popcll(m & ((1ull << lane) - 1ull))] = value;
 }
 
+// wave_append to two lists at once: both counters' atomics are issued before
+// either result is waited for.
+__device__ __forceinline__ void wave_append2(int32_t* cnt_a, int32_t* seg_a, bool mine_a,
+                                             int32_t* cnt_b, int32_t* seg_b, bool mine_b, int32_t value) {
+    const unsigned long long ma = __ballot(mine_a), mb = __ballot(mine_b);
+    if ((ma | mb) == 0ull) return;
+    const int lane = lane_id();
+    const int fa = ma ? __ffsll((long long)ma) - 1 : 0, fb = mb ? __ffsll((long long)mb) - 1 : 0;
+    int ba = 0, bb = 0;
+    if (ma && lane == fa) ba = atomicAdd(cnt_a, (int)__popcll(ma));
+    if (mb && lane == fb) bb = atomicAdd(cnt_b, (int)__popcll(mb));
+    ba = __shfl(ba, fa);
+    bb = __shfl(bb, fb);
+    const unsigned long long below = (1ull << lane) - 1ull;
+    if (mine_a) seg_a[ba + (int)__popcll(ma & below)] = value;
+    if (mine_b) seg_b[bb + (int)__popcll(mb & below)] = value;
+}
+
 __global__ __launch_bounds__(256) void pillar_update_kernel(PillarArgs a) {
     const int lane = lane_id(), wave = (int)(threadIdx.x >> 6);
     const int shard = (int)(blockIdx.x % NSHARD);
@@ -58,10 +76,13 @@ __global__ __launch_bounds__(256) void pillar_update_kernel(PillarArgs a) {
             const int c = v ? a.touched_pop[i] : 0;
             bool first = false;
             if (v) {
+                // both loads and the stamp in one round trip
                 const uint32_t k = a.scnt_pop[c];
+                const uint32_t h = a.head[c];
+                const uint32_t old = atomicMax(&a.stamp0[c], a.epoch);
                 a.scnt_pop[c] = 0u;
-                a.head[c] += k;
-                first = atomicMax(&a.stamp0[c], a.epoch) < a.epoch;
+                a.head[c] = h + k;
+                first = old < a.epoch;
             }
             wave_append(cnt0, seg0, first, c);
         }
@@ -78,14 +99,16 @@ __global__ __launch_bounds__(256) void pillar_update_kernel(PillarArgs a) {
             const int c = v ? (int)fy * a.W + (int)fx : 0;
             bool first_ins = false, first_chg = false;
             if (v) {
+                // the four atomics in one round trip, the ring store after
                 const uint32_t pos = atomicAdd(&a.tail[c], 1u);
-                a.ring[(size_t)c * a.N + pos % (uint32_t)a.N] = p;
                 atomicAdd(&a.scnt_ins[c], 1u);
-                first_ins = atomicMax(&a.ins_stamp[c], a.epoch) < a.epoch;
-                first_chg = atomicMax(&a.stamp0[c], a.epoch) < a.epoch;
+                const uint32_t oi = atomicMax(&a.ins_stamp[c], a.epoch);
+                const uint32_t oc = atomicMax(&a.stamp0[c], a.epoch);
+                a.ring[(size_t)c * a.N + pos % (uint32_t)a.N] = p;
+                first_ins = oi < a.epoch;
+                first_chg = oc < a.epoch;
             }
-            wave_append(a.tcount_ins, a.touched_ins, first_ins, c);
-            wave_append(cnt0, seg0, first_chg, c);
+            wave_append2(a.tcount_ins, a.touched_ins, first_ins, cnt0, seg0, first_chg, c);
         }
     }
 }
