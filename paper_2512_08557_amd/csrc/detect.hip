@@ -83,47 +83,60 @@ __device__ __forceinline__ void emit_rows(const DetectArgs& a, int p, int pc, bo
     if (mtog) memb_settle(a.memb, pc, a.next.Hin, a.next.Win, mb, md, a.epoch, got);
 }
 
-// Row i of the new list (present pass), valid while i < iend.  a.sorted: the
-// list was passed as increasing strictly; a row not above its predecessor is
-// an input fault.
-template <int ROWB, bool BF16, bool SPARSE>
-__device__ __forceinline__ void present_rows(const DetectArgs& a, int i, int iend, int shard) {
+// Rows i + u*step (u < U) of the new list (present pass), each valid while
+// below iend; a.count >= 1.  Every row's cell is loaded first, then every
+// row's canvas and feature pieces, so all U rows' loads are in flight
+// together before the first comparison.  a.sorted: the list was passed as
+// increasing strictly; a row not above its predecessor is an input fault.
+template <int ROWB, bool BF16, bool SPARSE, int U>
+__device__ __forceinline__ void present_rows(const DetectArgs& a, int i, int step, int iend, int shard) {
     constexpr int G = ROWB / 16;
     const int sub = lane_id() % G;
-    bool act = i < iend;
-    int p = -1;
-    if (act) {
-        p = a.idx ? a.idx[i] : i;
-        if (p < 0 || p >= a.HW) {
+    // loads are unconditional from clamped addresses (selected afterwards):
+    // a load inside a divergent branch makes the compiler drain all
+    // outstanding loads where the branch ends
+    int p[U], nx[U];
+    bool act[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int r = i + u * step;
+        act[u] = r < iend;
+        p[u] = a.idx ? a.idx[min(r, a.count - 1)] : r;
+        // the next row's cell, for the order check, in the same round trip
+        nx[u] = a.sorted ? a.idx[min(r + 1, a.count - 1)] : 0;
+    }
+    int pc[U];
+    uint64_t op[U];
+    uint4 ov[U], nv[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int r = i + u * step;
+        if (act[u] && (p[u] < 0 || p[u] >= a.HW)) {
             if (sub == 0) flag_error(a.err, ERR_INDEX_RANGE);
-            act = false;
+            act[u] = false;
         }
+        if (a.sorted && act[u] && sub == 0 && r + 1 < a.count && nx[u] <= p[u])
+            flag_error(a.err, nx[u] == p[u] ? ERR_DUPLICATE : ERR_UNSORTED);
+        // presence: a pillar marks its cell present for this stride (plain
+        // store; the vanish pass checks ownership).  The canvas and feature
+        // rows are fetched in the same round trip as the presence word.
+        pc[u] = act[u] ? p[u] : 0;
+        // sparse backbones: the pillar set itself is an input; a pillar
+        // whose cell had none in the previous stride appeared (the word was
+        // written by an earlier stride, or never)
+        op[u] = SPARSE ? a.pres[pc[u]] : 0ull;
+        if (act[u] && sub == 0) a.pres[p[u]] = ((uint64_t)a.epoch << 32) | (uint32_t)r;
+        ov[u] = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.X) + (size_t)pc[u] * ROWB + sub * 16);
+        nv[u] = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.feats) +
+                                                (size_t)min(r, a.count - 1) * ROWB + sub * 16);
     }
-    if (a.sorted) {
-        // the next row's cell, from a clamped position, in the same round trip
-        const int nx = a.idx[min(i + 1, a.count - 1)];
-        if (act && sub == 0 && i + 1 < a.count && nx <= p) flag_error(a.err, nx == p ? ERR_DUPLICATE : ERR_UNSORTED);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int r = i + u * step;
+        const bool tog = SPARSE && act[u] && (op[u] == 0ull || (uint32_t)(op[u] >> 32) != a.epoch - 1u);
+        if (a.prev_out && sub == 0 && r < iend) a.prev_out[r] = act[u] ? p[u] : -1;
+        emit_rows<ROWB, BF16, SPARSE>(a, p[u], pc[u], act[u], tog, nv[u], ov[u], shard, false);
     }
-    // presence: a pillar marks its cell present for this stride (plain
-    // store; the vanish pass checks ownership).  The canvas and feature rows
-    // are fetched in the same round trip as the presence word.  Loads are
-    // unconditional from clamped addresses (selected afterwards): a load
-    // inside a divergent branch makes the compiler drain all outstanding
-    // loads where the branch ends.
-    const int pc = act ? p : 0;
-    const uint64_t mine = ((uint64_t)a.epoch << 32) | (uint32_t)i;
-    // sparse backbones: the pillar set itself is an input; a pillar whose
-    // cell had none in the previous stride appeared (the word was written by
-    // an earlier stride, or never)
-    uint64_t op = 0ull;
-    if (SPARSE) op = a.pres[pc];
-    if (act && sub == 0) a.pres[p] = mine;
-    const uint4 ov = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.X) + (size_t)pc * ROWB + sub * 16);
-    const uint4 nv = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.feats) +
-                                                     (size_t)min(i, a.count - 1) * ROWB + sub * 16);
-    const bool tog = SPARSE && act && (op == 0ull || (uint32_t)(op >> 32) != a.epoch - 1u);
-    if (a.prev_out && sub == 0 && i < iend) a.prev_out[i] = act ? p : -1;
-    emit_rows<ROWB, BF16, SPARSE>(a, p, pc, act, tog, nv, ov, shard, false);
 }
 
 // A cell p known to have lost its pillar (valid when act): its old row
@@ -157,7 +170,7 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
     for (int base = wave * PPW; base < rows; base += nwaves * PPW) {
         const int i = base + lane / G;
         if constexpr (!VANISH) {
-            present_rows<ROWB, BF16, SPARSE>(a, i, a.count, shard);
+            present_rows<ROWB, BF16, SPARSE, 1>(a, i, 0, a.count, shard);
         } else {
             bool act = i < a.count;
             int p = -1;
@@ -208,6 +221,20 @@ __device__ __forceinline__ int lower_bound32(const int32_t* __restrict__ v, int 
     return L;
 }
 
+// Rows of the new list per workgroup of the sorted detection: the three
+// present wavefronts take U passes of PPW rows each (at most 64 rows, the
+// size of the previous-list chunk).  U = 1 while one pass per workgroup puts
+// the whole list into one round of resident workgroups; a longer list takes
+// UB passes, all their loads in flight together, so that it needs fewer
+// rounds of the chunk's dependent round trips (four 1024x1024 images: ~13k
+// chunks of 12 rows otherwise).
+template <int ROWB>
+struct SortedChunk {
+    static constexpr int PPW = 64 / (ROWB / 16);
+    static constexpr int UB = 3 * PPW >= 64 ? 1 : (64 / (3 * PPW) < 8 ? 64 / (3 * PPW) : 8);
+    static constexpr int rows(int u) { return 3 * PPW * u < 64 ? 3 * PPW * u : 64; }
+};
+
 // Sorted pillar lists (cells strictly increasing, the row-major order of a
 // pillar scatter): both passes in one launch, every comparison of the two
 // lists inside one workgroup.  Workgroup k takes rows k*CH .. of the new list
@@ -222,11 +249,12 @@ __device__ __forceinline__ int lower_bound32(const int32_t* __restrict__ v, int 
 // process them.  Each workgroup's work is bounded by its two chunks, so a
 // region that loses all its pillars at once spreads over the workgroups of
 // its stretch of the previous list.
-template <int ROWB, bool BF16, bool SPARSE>
+// U: rows of the new list per lane group and wavefront (SortedChunk).
+template <int ROWB, bool BF16, bool SPARSE, int U>
 __global__ __launch_bounds__(256) void detect_sorted_kernel(DetectArgs a) {
     constexpr int G = ROWB / 16;
     constexpr int PPW = 64 / G;
-    constexpr int CH = 3 * PPW < 64 ? 3 * PPW : 64;   // rows of the new list per workgroup
+    constexpr int CH = SortedChunk<ROWB>::rows(U);    // rows of the new list per workgroup
     __shared__ int vq[64];                            // the vanished cells of the workgroup's previous chunk
     __shared__ int nvq;
     const int lane = lane_id();
@@ -241,8 +269,8 @@ __global__ __launch_bounds__(256) void detect_sorted_kernel(DetectArgs a) {
     for (int k = (int)blockIdx.x; k < nchunk; k += (int)gridDim.x) {
         if (w < 3) {
             const int i0 = k * CH;
-            if (i0 < n && w * PPW < CH) present_rows<ROWB, BF16, SPARSE>(a, i0 + w * PPW + lane / G,
-                                                                              min(i0 + CH, n), shard);
+            if (i0 < n && w * PPW < CH)
+                present_rows<ROWB, BF16, SPARSE, U>(a, i0 + w * PPW + lane / G, 3 * PPW, min(i0 + CH, n), shard);
         } else {
             const int j0 = 64 * k;
             int nv = 0;
@@ -334,21 +362,35 @@ static hipError_t launch_detect(const DetectArgs& a, int row_bytes, bool bf16, c
 #undef SSC_DETECT_CASE
 }
 
-hipError_t launch_detect_sorted(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c) {
-    const int G = row_bytes / 16;
-    const int ch = std::min(3 * (64 / G), 64);
+// resident workgroups of detect_sorted_kernel (256 threads) on 256 compute units
+constexpr long long SORTED_ROUND = 2048;
+
+template <int RB>
+static hipError_t launch_ds(const DetectArgs& a, bool bf16, const LaunchCtx& c) {
+    using SC = SortedChunk<RB>;
+    const bool wide = (long long)a.count > SORTED_ROUND * SC::rows(1);
+    const int ch = SC::rows(wide ? SC::UB : 1);
     long long blocks = std::max(((long long)a.count + ch - 1) / ch, ((long long)a.prev_count + 63) / 64);
     if (blocks < 1) blocks = 1;
     if (blocks > 4096) blocks = 4096;
     dim3 grid((unsigned)blocks), block(256);
     const bool sp = a.memb.memb != nullptr;
-#define SSC_DETECT_CASE(RB)                                                                          \
-    case RB:                                                                                         \
-        if (sp)                                                                                      \
-            return bf16 ? launch_kernel(c, detect_sorted_kernel<RB, true, true>, grid, block, a)     \
-                        : launch_kernel(c, detect_sorted_kernel<RB, false, true>, grid, block, a);   \
-        return bf16 ? launch_kernel(c, detect_sorted_kernel<RB, true, false>, grid, block, a)        \
-                    : launch_kernel(c, detect_sorted_kernel<RB, false, false>, grid, block, a);
+    if (wide) {
+        if (sp) return bf16 ? launch_kernel(c, detect_sorted_kernel<RB, true, true, SC::UB>, grid, block, a)
+                            : launch_kernel(c, detect_sorted_kernel<RB, false, true, SC::UB>, grid, block, a);
+        return bf16 ? launch_kernel(c, detect_sorted_kernel<RB, true, false, SC::UB>, grid, block, a)
+                    : launch_kernel(c, detect_sorted_kernel<RB, false, false, SC::UB>, grid, block, a);
+    }
+    if (sp) return bf16 ? launch_kernel(c, detect_sorted_kernel<RB, true, true, 1>, grid, block, a)
+                        : launch_kernel(c, detect_sorted_kernel<RB, false, true, 1>, grid, block, a);
+    return bf16 ? launch_kernel(c, detect_sorted_kernel<RB, true, false, 1>, grid, block, a)
+                : launch_kernel(c, detect_sorted_kernel<RB, false, false, 1>, grid, block, a);
+}
+
+hipError_t launch_detect_sorted(const DetectArgs& a, int row_bytes, bool bf16, const LaunchCtx& c) {
+#define SSC_DETECT_CASE(RB) \
+    case RB:                \
+        return launch_ds<RB>(a, bf16, c);
     switch (row_bytes) {
         SSC_DETECT_CASE(16)
         SSC_DETECT_CASE(32)

@@ -50,8 +50,11 @@ def _compare(beng, sengs, L, where):
 
 
 def test_four_stream_drone_grid_in_one_handle():
-    """The four 1024x1024 streams in one batched handle (the bench's default
-    launch configuration for this workload) over the full 100 delta strides:
+    """The four 1024x1024 streams in one batched handle with the one-launch
+    detection of its sorted pillar list (the bench's default launch
+    configuration for this workload; ~160k pillars, so the multi-pass chunks)
+    over the full 100 delta strides, against handles of their own that take
+    the two detection passes:
     every 10th stride each image equals a handle of its own bit for bit, and
     every 20th stride and the last one image (in turn) is checked against the
     oracle."""
@@ -65,7 +68,7 @@ def test_four_stream_drone_grid_in_one_handle():
         note(f"[gpu-test] c5 batched stride {t}")
         for b in range(B):
             sengs[b].step(*to_device(gens[b][t], wl.dtype))
-        beng.step(*to_device(_stack([g[t] for g in gens], wl.H, wl.W), wl.dtype))
+        beng.step(*to_device(_stack([g[t] for g in gens], wl.H, wl.W), wl.dtype), sorted=True)
         if t % 10 == 0 or t == n:
             _compare(beng, sengs, len(wl.layers), f"stride {t}")
         if t % 20 == 0 or t == n:

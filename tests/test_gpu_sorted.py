@@ -53,12 +53,17 @@ def _same(e1, e2, n_layers, where):
 
 
 # (H, W, C0, layers, dtype): chunks of 48 rows (fp32 C0 = 16), 12 (fp32 C0 = 64)
-# and 64 (bf16 C0 = 16) pillars
+# and 64 (bf16 C0 = 16) pillars.  The two large grids hold more pillars than
+# 2048 one-pass chunks (24,576 fp32 rows of 64 channels, 49,152 bf16 ones), so
+# their strides take the multi-pass chunks (60 and 48 rows), except where most
+# pillars vanish
 GRIDS = [
     (37, 23, 16, [(16, 32, 1, True), (32, 32, 2, True)], "f32"),
     (29, 31, 64, [(64, 64, 2, True), (64, 128, 1, True), (128, 128, 1, True)], "f32"),
     (40, 40, 16, [(16, 16, 1, True), (16, 32, 2, False)], "bf16"),
     (5, 300, 64, [(64, 64, 1, True)], "bf16"),
+    (300, 300, 64, [(64, 64, 1, True)], "f32"),
+    (420, 420, 64, [(64, 64, 2, True)], "bf16"),
 ]
 
 

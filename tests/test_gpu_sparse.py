@@ -148,3 +148,44 @@ def test_sparse_handle_refuses_dense_steps():
         eng.step(None, dense)
     assert ei.value.code == -1
     eng.close()
+
+
+def test_sorted_large_list_matches_two_pass_bitwise():
+    """A sparse handle fed sorted lists longer than 2048 one-pass chunks of
+    the one-launch detection (300x300 fp32, 64 channels, ~30k pillars: the
+    multi-pass chunks; regular, regular, submanifold layers), pillars
+    appearing and vanishing and some carrying zeros, against a handle that takes the two detection passes: lists,
+    active counts and maps bit for bit at every stride."""
+    H, W, C0 = 300, 300, 64
+    layers = [(64, 64, 1, True), (64, 64, 1, True), (64, 64, 1, True)]
+    sub = [False, False, True]
+    rng = np.random.default_rng(300)
+    ws = [(rng.standard_normal((co, ci, 3, 3)) * np.sqrt(2.0 / (9 * ci))).astype(np.float32)
+          for (ci, co, _s, _r) in layers]
+    e1 = _engine(H, W, C0, layers, ws, sub, "f32", H * W)
+    e2 = _engine(H, W, C0, layers, ws, sub, "f32", H * W)
+    occ = rng.random(H * W) < 0.35
+    feat = rng.standard_normal((H * W, C0)).astype(np.float32)
+    for t in range(10):
+        if t:
+            occ = occ ^ (rng.random(H * W) < 0.05)
+            r = rng.random(H * W) < 0.08
+            feat[r] = rng.standard_normal((int(r.sum()), C0))
+        if t == 6:
+            occ = occ & (rng.random(H * W) < 0.2)     # most pillars vanish: one-pass chunks
+        feat[occ & (rng.random(H * W) < 0.03)] = 0.0
+        idx = np.flatnonzero(occ).astype(np.int32)
+        st = S.Stride(t, idx, feat[idx].copy())
+        d = to_device(st, "f32")
+        e1.step(*d, sorted=True)
+        e2.step(*d)
+        where = f"stride {t} P={len(idx)}"
+        for l in range(len(layers) + 1):
+            a, b = e1.changed(l), e2.changed(l)
+            assert np.array_equal(a, b), f"{where}: A_{l} differs ({len(a)} vs {len(b)})"
+        s1, s2 = e1.stats(), e2.stats()
+        assert s1["active"] == s2["active"], where
+        for l in range(len(layers) + 1):
+            assert torch.equal(e1.read(l).view(torch.int32), e2.read(l).view(torch.int32)), f"{where}: map {l}"
+    e1.close()
+    e2.close()
