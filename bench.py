@@ -336,8 +336,10 @@ def short_kernel(name: str) -> str:
     fn, _, targs = base.partition("<")
     t = [x.strip() for x in targs.rstrip(">").split(",")]
     dt = lambda v: "bf16" if v == "true" else "f32"
-    if fn == "detect_sorted_kernel" and len(t) == 3:
-        return f"detect_sorted_kernel<{t[0]},{dt(t[1])}>"
+    if fn == "detect_sorted_kernel" and len(t) in (3, 4):
+        # the fourth argument: rows per lane group and wavefront (several for long lists)
+        passes = f",{t[3]} passes" if len(t) == 4 and t[3] != "1" else ""
+        return f"detect_sorted_kernel<{t[0]},{dt(t[1])}{passes}>"
     if fn == "detect_kernel" and len(t) in (3, 4):
         return f"detect_kernel<{t[0]},{dt(t[1])},{'vanished' if t[2] == 'true' else 'present'}>"
     if fn in ("layer_kernel", "layer_kernel_wide") and len(t) in (4, 5, 6):

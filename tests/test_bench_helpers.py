@@ -95,6 +95,10 @@ def test_detection_slot_names_follow_the_detection_form(monkeypatch):
     assert bench.kernel_name(1, wl) == "detect_kernel<vanished>"
     assert bench.short_kernel("void ssc::detect_sorted_kernel<256, false, false>(ssc::DetectArgs)") == \
         "detect_sorted_kernel<256,f32>"
+    assert bench.short_kernel("void ssc::detect_sorted_kernel<256, false, true, 1>(ssc::DetectArgs)") == \
+        "detect_sorted_kernel<256,f32>"
+    assert bench.short_kernel("void ssc::detect_sorted_kernel<128, true, false, 2>(ssc::DetectArgs)") == \
+        "detect_sorted_kernel<128,bf16,2 passes>"
     assert bench.short_kernel("void ssc::detect_kernel<128, true, true, false>(ssc::DetectArgs)") == \
         "detect_kernel<128,bf16,vanished>"
     assert bench.launches_per_stride("detect_sorted_kernel<256,f32>", wl) == 1
