@@ -63,7 +63,10 @@ namespace ssc {
 // them over CS workgroups per tile, one block per wavefront each, on the same
 // XCD: its output list is ~4x shorter than its input list (the c3/c4 layer
 // 64->128: ~80 tiles, fewer than the compute units), so a wavefront's matrix
-// work is the chain that ends the launch.  (Stride 1 with ~170 tiles: the
+// work is the chain that ends the launch.  With four blocks (cout 64) the
+// tile's two workgroups take two blocks each: twice the compute units, each
+// streaming half the tile's operands (block 1's first layer: 68 tiles on
+// 432x496, 0.5-1 us shorter per launch).  (Stride 1 with ~170 tiles: the
 // split only doubles the gathers; measured 1 us slower per launch.)
 // bf16 weights: the pair form contracts [Y_new | Y_old] against [W | -W];
 // the packed weights hold W once (chunk c of the pair uses weight chunk
@@ -86,7 +89,8 @@ __device__ __forceinline__ uint4 old_half_negated(uint4 v, int c, int g) {
 template <int COUT, int S = 1>
 struct LayerShape {
     static constexpr int NCBT = (COUT + 15) / 16;           // 16-wide cout blocks
-    static constexpr int CS = S == 2 && NCBT > 4 ? NCBT / 4 : 1;   // workgroups per tile (cout parts)
+    // workgroups per tile (cout parts)
+    static constexpr int CS = S == 2 ? (NCBT > 4 ? NCBT / 4 : (NCBT == 4 ? 2 : 1)) : 1;
     static constexpr int NCBW = NCBT / CS;                  // cout blocks per workgroup
     static constexpr int NWC = NCBW >= 4 ? 4 : NCBW;        // wavefronts across the cout blocks
     static constexpr int KS = NWC == 1 ? 4 : 1;             // wavefronts across the contraction
