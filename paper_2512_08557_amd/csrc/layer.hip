@@ -60,8 +60,8 @@ namespace ssc {
 // their partial sums through LDS (measured: a 2-way split at COUT = 32 is
 // slower than 2 wavefronts with the whole contraction each).
 // A stride-2 layer with more than four blocks (cout 128 and 256) spreads
-// them over CS workgroups per tile, one block per wavefront each, on the same
-// XCD: its output list is ~4x shorter than its input list (the c3/c4 layer
+// them over CS workgroups per tile, one block per wavefront each (four per
+// workgroup, two for bf16 and sparse layers), on the same XCD: its output list is ~4x shorter than its input list (the c3/c4 layer
 // 64->128: ~80 tiles, fewer than the compute units), so a wavefront's matrix
 // work is the chain that ends the launch.  With four blocks (cout 64) the
 // tile's two workgroups take two blocks each: twice the compute units, each
@@ -86,11 +86,14 @@ __device__ __forceinline__ uint4 old_half_negated(uint4 v, int c, int g) {
     return make_uint4(v.x ^ s, v.y ^ s, v.z ^ s, v.w ^ s);
 }
 
-template <int COUT, int S = 1>
+// FINE: bf16 or sparse layers, whose stride-2 tiles with more than four
+// blocks spread over workgroups of two blocks (measured faster there; four
+// blocks per workgroup measured faster for dense fp32 layers).
+template <int COUT, int S = 1, bool FINE = false>
 struct LayerShape {
     static constexpr int NCBT = (COUT + 15) / 16;           // 16-wide cout blocks
     // workgroups per tile (cout parts)
-    static constexpr int CS = S == 2 ? (NCBT > 4 ? NCBT / 4 : (NCBT == 4 ? 2 : 1)) : 1;
+    static constexpr int CS = S == 2 ? (NCBT > 4 ? NCBT / (FINE ? 2 : 4) : (NCBT == 4 ? 2 : 1)) : 1;
     static constexpr int NCBW = NCBT / CS;                  // cout blocks per workgroup
     static constexpr int NWC = NCBW >= 4 ? 4 : NCBW;        // wavefronts across the cout blocks
     static constexpr int KS = NWC == 1 ? 4 : 1;             // wavefronts across the contraction
@@ -124,10 +127,10 @@ __device__ __forceinline__ void mfma_chunk(f4v (&acc)[NCB], const uint4 av, cons
 // SPREAD (with SPARSE): the layer is regular and the next regular layer's
 // active-set counts follow its sites (a.mnext set).
 template <int CIN, int COUT, int S, bool BF16, bool SPARSE, bool SPREAD>
-__global__ __launch_bounds__((64 * LayerShape<COUT, S>::NW)) void layer_kernel(const int32_t* __restrict__ plist,
+__global__ __launch_bounds__((64 * LayerShape<COUT, S, BF16 || SPARSE>::NW)) void layer_kernel(const int32_t* __restrict__ plist,
                                                                           const int32_t* __restrict__ pcount, int pcap,
                                                                           LayerArgs a) {
-    using LS = LayerShape<COUT, S>;
+    using LS = LayerShape<COUT, S, BF16 || SPARSE>;
     constexpr int NCBT = LS::NCBT;
     constexpr int NCB = LS::NCB;
     constexpr int NWC = LS::NWC, KS = LS::KS;
@@ -591,13 +594,14 @@ static hipError_t launch_shape(const LayerArgs& a, int grid, const LaunchCtx& c)
                              a.list, a.count, a.cap, a);
     } else {
         // whole runs of 4 tiles on every XCD for every segment and cout part
-        constexpr int GU = 32 * NSHARD * LayerShape<CO, S>::CS;
+        using LS = LayerShape<CO, S, BF16 || SPARSE>;
+        constexpr int GU = 32 * NSHARD * LS::CS;
         grid = std::max(GU, grid / GU * GU);
         if constexpr (SPARSE)
             if (a.mnext.memb)
                 return launch_kernel(c, layer_kernel<CI, CO, S, BF16, true, true>, dim3(grid),
-                                     dim3(64 * LayerShape<CO, S>::NW), a.list, a.count, a.cap, a);
-        return launch_kernel(c, layer_kernel<CI, CO, S, BF16, SPARSE, false>, dim3(grid), dim3(64 * LayerShape<CO, S>::NW),
+                                     dim3(64 * LS::NW), a.list, a.count, a.cap, a);
+        return launch_kernel(c, layer_kernel<CI, CO, S, BF16, SPARSE, false>, dim3(grid), dim3(64 * LS::NW),
                              a.list, a.count, a.cap, a);
     }
 }
