@@ -103,7 +103,9 @@ struct sscater {
     int32_t prev_count = 0;
     bool prev_dense = false;
     bool prev_sorted = true;       // the previous list is known to increase (or is empty)
-    int32_t* counters = nullptr;   // [2][2*(L+1)][NSHARD][CSTRIDE]: per set cnt[0..L][shard], pairs[0..L][shard]
+    // [2 sets][nlines()][CSTRIDE], word 0 of each line a counter: per set the
+    // list lengths cnt[0..L][shard], then pairs[0..L][shard][PSPREAD]
+    int32_t* counters = nullptr;
     long long* cum = nullptr;      // running totals, same layout as one set
     int32_t* err_host = nullptr;   // host-visible sticky error word
     int32_t* err_dev = nullptr;
@@ -138,13 +140,16 @@ struct sscater {
     size_t ev_next = 0;
     std::vector<ProfRec> prof_recs;
 
-    int ncnt() const { return 2 * (L + 1) * NSHARD * CSTRIDE; }
+    int nlines() const { return (L + 1) * NSHARD * (1 + PSPREAD); }
+    int ncnt() const { return nlines() * CSTRIDE; }
     // cells of layer l's output grid over the whole batch (l = 0: the input)
     size_t cells_of(int l) const {
         return (size_t)batch * (l == 0 ? (size_t)grid.H * grid.W : (size_t)layers[l - 1].Hout * layers[l - 1].Wout);
     }
     int32_t* cnt_ptr(int set, int l) { return set_ptr(set) + (size_t)l * NSHARD * CSTRIDE; }
-    int32_t* pairs_ptr(int set, int l) { return set_ptr(set) + (size_t)(L + 1 + l) * NSHARD * CSTRIDE; }
+    int32_t* pairs_ptr(int set, int l) {
+        return set_ptr(set) + ((size_t)(L + 1) * NSHARD + (size_t)l * NSHARD * PSPREAD) * CSTRIDE;
+    }
     int32_t* set_ptr(int s) { return counters + (size_t)s * ncnt(); }
 };
 
@@ -269,7 +274,7 @@ int run_layers(sscater* h, int set, uint32_t epoch, hipStream_t s) {
         if (l == h->L) {
             a.cum_src = cnt;
             a.cum_dst = h->cum;
-            a.n_cum = h->ncnt();
+            a.n_cum = h->nlines();
         }
         if (ls.split) {
             ContractArgs g{};
@@ -580,7 +585,7 @@ static int step_impl(sscater_t h, const sscater_pillars* pl, void* stream, bool 
     d.count0 = h->cnt_ptr(set, 0);
     d.delta0 = h->delta0;
     d.zero_ptr = h->set_ptr(set ^ 1);
-    d.zero_n = h->ncnt();
+    d.zero_n = h->nlines();
     d.HW = (int32_t)cells;
     d.epoch = epoch;
     d.err = h->err_dev;
@@ -734,7 +739,7 @@ int sscater_step_points(sscater_t h, const float* points, int32_t n_points, void
     u.list0 = h->list0;
     u.count0 = h->cnt_ptr(set, 0);
     u.zero_ptr = h->set_ptr(set ^ 1);
-    u.zero_n = h->ncnt();
+    u.zero_n = h->nlines();
     u.epoch = epoch;
     // the leaving stride touched at most max_new_points cells
     u.n_pop_blocks = std::max(1, std::min(64, (p.max_new_points + 255) / 256));
@@ -1011,9 +1016,12 @@ int sscater_stats(sscater_t h, sscater_stats_t* out, void* stream) {
         long long a_c = 0, p_c = 0, a_t = 0, p_t = 0;
         for (int k = 0; k < NSHARD; ++k) {
             a_c += c[((size_t)l * NSHARD + k) * CSTRIDE];
-            p_c += c[((size_t)(L + 1 + l) * NSHARD + k) * CSTRIDE];
             a_t += t[((size_t)l * NSHARD + k) * CSTRIDE];
-            p_t += t[((size_t)(L + 1 + l) * NSHARD + k) * CSTRIDE];
+            for (int x = 0; x < PSPREAD; ++x) {
+                const size_t line = (size_t)(L + 1) * NSHARD + ((size_t)l * NSHARD + k) * PSPREAD + x;
+                p_c += c[line * CSTRIDE];
+                p_t += t[line * CSTRIDE];
+            }
         }
         act[l] = a_c;
         prs[l] = p_c;

@@ -250,7 +250,8 @@ __global__ __launch_bounds__(256) void tap_sum_kernel(const int32_t* __restrict_
     const int n = pcount[shard * CSTRIDE];
 
     if (a.cum_dst && b == 0)
-        for (int i = (int)threadIdx.x; i < a.n_cum; i += (int)blockDim.x) a.cum_dst[i] += a.cum_src[i];
+        for (int i = (int)threadIdx.x; i < a.n_cum; i += (int)blockDim.x)
+            a.cum_dst[(size_t)i * CSTRIDE] += a.cum_src[(size_t)i * CSTRIDE];
 
     const int sub = lane & 15;                   // propagation: tap slot of the lane
     const int cp = 4 * w + (lane >> 4);          // propagation: cell of the lane (cp < TC)

@@ -162,7 +162,7 @@ __global__ __launch_bounds__(256) void detect_kernel(DetectArgs a) {
     const int sub = lane % G;
 
     if (!VANISH && a.zero_ptr && blockIdx.x == 0)
-        for (int i = threadIdx.x; i < a.zero_n; i += blockDim.x) a.zero_ptr[i] = 0;
+        for (int i = threadIdx.x; i < a.zero_n; i += blockDim.x) a.zero_ptr[(size_t)i * CSTRIDE] = 0;
 
     const int wave = (int)((blockIdx.x * blockDim.x + threadIdx.x) >> 6);
     const int nwaves = (int)((gridDim.x * blockDim.x) >> 6);
@@ -264,7 +264,7 @@ __global__ __launch_bounds__(256) void detect_sorted_kernel(DetectArgs a) {
     const int nchunk = max(max((n + CH - 1) / CH, (m + 63) / 64), 1);
 
     if (a.zero_ptr && blockIdx.x == 0)
-        for (int i = threadIdx.x; i < a.zero_n; i += blockDim.x) a.zero_ptr[i] = 0;
+        for (int i = threadIdx.x; i < a.zero_n; i += blockDim.x) a.zero_ptr[(size_t)i * CSTRIDE] = 0;
 
     for (int k = (int)blockIdx.x; k < nchunk; k += (int)gridDim.x) {
         if (w < 3) {

@@ -85,7 +85,7 @@ __device__ __forceinline__ void prop_finish(const PropTarget& t, uint32_t epoch,
     int base = 0;
     if (lane == 0) {
         if (tot) base = atomicAdd(t.count + shard * CSTRIDE, tot);
-        if (pairs) atomicAdd(t.pairs + shard * CSTRIDE, pairs);
+        if (pairs) atomicAdd(t.pairs + (shard * PSPREAD + (int)(blockIdx.x & (PSPREAD - 1))) * CSTRIDE, pairs);
     }
     if (tot == 0) return;
     base = __shfl(base, 0);
@@ -243,7 +243,7 @@ __device__ __forceinline__ void prop_reserve(const PropTarget& t, uint32_t epoch
     }
     if (lane_id() == 0) {
         if (ps.tot) ps.base = atomicAdd(t.count + shard * CSTRIDE, ps.tot);
-        if (pairs) atomicAdd(t.pairs + shard * CSTRIDE, pairs);
+        if (pairs) atomicAdd(t.pairs + (shard * PSPREAD + (int)(blockIdx.x & (PSPREAD - 1))) * CSTRIDE, pairs);
     }
 }
 

@@ -171,7 +171,8 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S, BF16 || SPARSE>::NW)) voi
     int qspec = seg[min(e, pcap - 1)];
 
     if (a.cum_dst && b == 0)
-        for (int i = (int)threadIdx.x; i < a.n_cum; i += (int)blockDim.x) a.cum_dst[i] += a.cum_src[i];
+        for (int i = (int)threadIdx.x; i < a.n_cum; i += (int)blockDim.x)
+            a.cum_dst[(size_t)i * CSTRIDE] += a.cum_src[(size_t)i * CSTRIDE];
 
     const bool do_prop = a.has_next && wave == 0 && part == 0;
     while (tile * 16 < n) {
@@ -559,7 +560,8 @@ __global__ __launch_bounds__((256 * WideGroups<CIN, COUT, S, BF16>::KH)) void la
         __syncthreads();                               // the stages and partial sums are free again
     }
     if (a.cum_dst && b == 0)
-        for (int i = (int)threadIdx.x; i < a.n_cum; i += (int)blockDim.x) a.cum_dst[i] += a.cum_src[i];
+        for (int i = (int)threadIdx.x; i < a.n_cum; i += (int)blockDim.x)
+            a.cum_dst[(size_t)i * CSTRIDE] += a.cum_src[(size_t)i * CSTRIDE];
 }
 
 // ---------------------------------------------------------------------------

@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256) void pillar_update_kernel(PillarArgs a) {
     int32_t* cnt0 = a.count0 + shard * CSTRIDE;
     int32_t* seg0 = a.list0 + (size_t)shard * ((size_t)a.H * a.W);
     if (a.zero_ptr && blockIdx.x == 0)
-        for (int i = (int)threadIdx.x; i < a.zero_n; i += (int)blockDim.x) a.zero_ptr[i] = 0;
+        for (int i = (int)threadIdx.x; i < a.zero_n; i += (int)blockDim.x) a.zero_ptr[(size_t)i * CSTRIDE] = 0;
 
     if ((int)blockIdx.x < a.n_pop_blocks) {
         // the stride leaving the window: its cells are unique in its list

@@ -23,6 +23,12 @@ constexpr int NSHARD = 2;
 // Distance between the counters of two segments (in int32): one 128-byte line
 // each, since atomics on different words of one line still queue together.
 constexpr int CSTRIDE = 32;
+// The pairs counter of a (layer, segment) is spread over PSPREAD lines, one per
+// XCD of the adding workgroup, and summed by the host: every wavefront that
+// appends to a list also adds its pairs, and on one line those adds queue
+// behind each other on the list builders' critical path.
+constexpr int PSPREAD = 8;
+static_assert((PSPREAD & (PSPREAD - 1)) == 0, "PSPREAD indexes by blockIdx.x & (PSPREAD - 1)");
 
 // Change-list propagation target: the next layer's grid and its list state.
 // A handle may hold a batch of independent images: cell index
@@ -35,7 +41,8 @@ struct PropTarget {
     uint32_t* stamp;      // [Hout*Wout]
     int32_t* list;        // NSHARD segments of Hout*Wout entries
     int32_t* count;       // segment lengths, segment k at count[k * CSTRIDE]
-    int32_t* pairs;       // (input, output) pairs of the consuming layer, same layout
+    int32_t* pairs;       // (input, output) pairs of the consuming layer: segment k,
+                          // XCD x at pairs[(k * PSPREAD + x) * CSTRIDE]
 };
 
 // Sparse backbones (regular sparse and submanifold convolutions): every
@@ -72,7 +79,7 @@ struct DetectArgs {
     int32_t* count0;      // |A_0| counters, shard k at count0[k * CSTRIDE]
     void* delta0;         // input deltas, dense by cell [H0*W0][4*C0 bytes]
     int32_t* zero_ptr;    // counters to clear for the next stride (may be nullptr)
-    int32_t zero_n;
+    int32_t zero_n;       // their lines (word 0 of each CSTRIDE line is the counter)
     int32_t HW;
     uint32_t epoch;
     int32_t* err;         // sticky error flags (host-visible memory)
@@ -102,8 +109,8 @@ struct LayerArgs {
     const uint64_t* memb;
     MembTarget mnext;
     // running totals, folded in by the last layer of a stride
-    const int32_t* cum_src;     // this stride's counters [n_cum]
-    long long* cum_dst;         // totals [n_cum]
+    const int32_t* cum_src;     // this stride's counters, word 0 of n_cum CSTRIDE lines
+    long long* cum_dst;         // totals, the same layout
     int n_cum;
     // layers contracted in two launches (tap_sum_kernel): the tap
     // contributions of the changed input cells, dense by cell
@@ -164,7 +171,7 @@ struct PillarArgs {
     int32_t* list0;             // A_0 list, NSHARD segments of H*W
     int32_t* count0;            // its counters, segment k at [k * CSTRIDE]
     int32_t* zero_ptr;          // counter set of the next stride, cleared here
-    int zero_n;
+    int zero_n;                 // its lines
     uint32_t epoch;
     int n_pop_blocks;           // workgroups [0, n_pop_blocks) remove, the others insert
 };
