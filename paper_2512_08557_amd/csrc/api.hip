@@ -104,7 +104,9 @@ struct sscater {
     bool prev_dense = false;
     bool prev_sorted = true;       // the previous list is known to increase (or is empty)
     // [2 sets][nlines()][CSTRIDE], word 0 of each line a counter: per set the
-    // list lengths cnt[0..L][shard], then pairs[0..L][shard][PSPREAD]
+    // list lengths cnt[0..L][shard], then pairs[0..L][shard][PSPREAD], then the
+    // detection's |A_0| adds [shard][PSPREAD] (statistics; points mode counts
+    // A_0 in cnt[0], the length of the list it builds)
     int32_t* counters = nullptr;
     long long* cum = nullptr;      // running totals, same layout as one set
     int32_t* err_host = nullptr;   // host-visible sticky error word
@@ -140,7 +142,7 @@ struct sscater {
     size_t ev_next = 0;
     std::vector<ProfRec> prof_recs;
 
-    int nlines() const { return (L + 1) * NSHARD * (1 + PSPREAD); }
+    int nlines() const { return (L + 1) * NSHARD * (1 + PSPREAD) + NSHARD * PSPREAD; }
     int ncnt() const { return nlines() * CSTRIDE; }
     // cells of layer l's output grid over the whole batch (l = 0: the input)
     size_t cells_of(int l) const {
@@ -150,6 +152,7 @@ struct sscater {
     int32_t* pairs_ptr(int set, int l) {
         return set_ptr(set) + ((size_t)(L + 1) * NSHARD + (size_t)l * NSHARD * PSPREAD) * CSTRIDE;
     }
+    int32_t* a0_ptr(int set) { return set_ptr(set) + (size_t)(L + 1) * NSHARD * (1 + PSPREAD) * CSTRIDE; }
     int32_t* set_ptr(int s) { return counters + (size_t)s * ncnt(); }
 };
 
@@ -582,7 +585,7 @@ static int step_impl(sscater_t h, const sscater_pillars* pl, void* stream, bool 
     d.X = h->X;
     d.pres = h->pres;
     d.stamp0 = h->stamp0;
-    d.count0 = h->cnt_ptr(set, 0);
+    d.count0 = h->a0_ptr(set);
     d.delta0 = h->delta0;
     d.zero_ptr = h->set_ptr(set ^ 1);
     d.zero_n = h->nlines();
@@ -1017,6 +1020,12 @@ int sscater_stats(sscater_t h, sscater_stats_t* out, void* stream) {
         for (int k = 0; k < NSHARD; ++k) {
             a_c += c[((size_t)l * NSHARD + k) * CSTRIDE];
             a_t += t[((size_t)l * NSHARD + k) * CSTRIDE];
+            if (l == 0)
+                for (int x = 0; x < PSPREAD; ++x) {
+                    const size_t line = (size_t)(L + 1) * NSHARD * (1 + PSPREAD) + (size_t)k * PSPREAD + x;
+                    a_c += c[line * CSTRIDE];
+                    a_t += t[line * CSTRIDE];
+                }
             for (int x = 0; x < PSPREAD; ++x) {
                 const size_t line = (size_t)(L + 1) * NSHARD + ((size_t)l * NSHARD + k) * PSPREAD + x;
                 p_c += c[line * CSTRIDE];

@@ -78,7 +78,8 @@ __device__ __forceinline__ void emit_rows(const DetectArgs& a, int p, int pc, bo
     if (mtog) memb_swap(a.memb, pc, a.next.Hin, a.next.Win, mb, md, a.epoch, got);
     // |A_0|: one counter per shard, no returned value to wait for
     const int changed = (int)__popcll(__ballot(gd && sub == 0));
-    if (lane == 0 && changed) atomicAdd(a.count0 + shard * CSTRIDE, changed);
+    if (lane == 0 && changed)
+        atomicAdd(a.count0 + (shard * PSPREAD + (int)(blockIdx.x & (PSPREAD - 1))) * CSTRIDE, changed);
     prop_finish<G>(a.next, a.epoch, shard, pb);
     if (mtog) memb_settle(a.memb, pc, a.next.Hin, a.next.Win, mb, md, a.epoch, got);
 }

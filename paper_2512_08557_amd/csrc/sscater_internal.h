@@ -76,7 +76,7 @@ struct DetectArgs {
     const int32_t* chk_idx;   // vanish mode: this stride's pillar list, checked for duplicate cells (may be nullptr)
     int32_t chk_count;
     uint32_t* stamp0;     // change stamps of the input grid [H0*W0]
-    int32_t* count0;      // |A_0| counters, shard k at count0[k * CSTRIDE]
+    int32_t* count0;      // |A_0| (statistics only): segment k, XCD x at count0[(k * PSPREAD + x) * CSTRIDE]
     void* delta0;         // input deltas, dense by cell [H0*W0][4*C0 bytes]
     int32_t* zero_ptr;    // counters to clear for the next stride (may be nullptr)
     int32_t zero_n;       // their lines (word 0 of each CSTRIDE line is the counter)
