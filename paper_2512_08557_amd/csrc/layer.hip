@@ -140,7 +140,6 @@ __global__ __launch_bounds__((64 * LayerShape<COUT, S, BF16 || SPARSE>::NW)) voi
     constexpr int NCH = KTOT / KCH;
     constexpr int NCHW = WeightChunks<CIN, BF16>::N;   // weight chunks per tap
     constexpr int ROWB_IN = 4 * CIN;             // input delta row bytes (fp32, or bf16 pair)
-    constexpr int ROWB_OUT = 4 * COUT;
 
     const int lane = (int)(threadIdx.x & 63u), wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
     const int cl = lane & 15, g = lane >> 4;
@@ -465,18 +464,21 @@ __global__ __launch_bounds__((256 * WideGroups<CIN, COUT, S, BF16>::KH)) void la
         if (lane == 0 && mask) atomicOr(&tapmask, (int)mask);
         __syncthreads();
         const unsigned taps = (unsigned)__builtin_amdgcn_readfirstlane(tapmask);
-        // this group's taps: every KH-th active one from the kh-th on
+        // this group's taps: those with t % KH == kh.  Fixed by the tap index,
+        // not by its rank among the tile pair's active taps, so that a cell's
+        // partial sums are grouped the same whichever cells share its tile
+        // pair (the list order, and with it the pairing, is set by atomics):
+        // the maps stay bit-identical from run to run
         unsigned mine = 0u;
-        {
-            int k = 0;
+        int nsteps = 0;
 #pragma unroll
-            for (int t = 0; t < 9; ++t)
-                if ((taps >> t) & 1u) {
-                    if (k % KH == kh) mine |= 1u << t;
-                    ++k;
-                }
+        for (int k = 0; k < KH; ++k) {
+            unsigned mk = 0u;
+#pragma unroll
+            for (int t = k; t < 9; t += KH) mk |= taps & (1u << t);
+            if (k == kh) mine = mk;
+            nsteps = max(nsteps, __builtin_popcount(mk));
         }
-        const int nsteps = (__builtin_popcount(taps) + KH - 1) / KH;
 
         // copies of tap t into the group's stage: the two wavefronts of a
         // tile share its delta chunks, the two wavefronts of a cout block its
