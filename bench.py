@@ -990,8 +990,10 @@ def main() -> int:
                                              "scaled by a plain copy)"})
 
     # ---- floor: strides whose input equals the previous one bit for bit ----
-    # every launch of a stride runs and finds an empty list: the fixed cost of
-    # the stride's launch chain, beside the work-carrying strides above
+    # every launch of a stride runs and finds an empty list.  The per-launch
+    # event times are the GPU's fixed cost per launch; the wall clock of such
+    # strides is bound by the host's enqueue of the chain (the GPU finishes
+    # right after the last call), unlike the work-carrying strides above
     floor = None
     if not args.no_profile:
         last_k = first + W + K - 1
